@@ -1,0 +1,173 @@
+"""Oracle tree metadata pinned to hand-derived values, closed forms and an
+independent brute force (boolean transitive closure), Sec. 3.4.1-3.4.2."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2607_06763_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "trees.txt")
+
+
+def _read_golden():
+    cases, invalid = {}, []
+    cur = None
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("invalid"):
+                st, arr = line[len("invalid"):].split(":")
+                invalid.append((int(st), [int(x) for x in arr.split()]))
+                continue
+            tok = line.split()
+            if tok[0] == "case":
+                cur = {"name": tok[1], "checks": []}
+                cases[tok[1]] = cur
+            elif tok[0] == "end":
+                cur = None
+            elif tok[0] == "check":
+                cur["checks"].append((int(tok[1]), int(tok[3]), [int(x) for x in tok[5:]]))
+            else:
+                cur[tok[0]] = [int(x) for x in tok[1:]]
+    return cases, invalid
+
+
+def _closure_meta(parent):
+    """Brute force, independent of the oracle: ancestor sets as the transitive
+    closure of the child->parent adjacency by repeated boolean squaring; depth
+    = number of proper ancestors; order by numpy lexsort."""
+    T = len(parent)
+    A = np.zeros((T, T), dtype=bool)
+    for i, p in enumerate(parent):
+        if p >= 0:
+            A[i, p] = True
+    R = A.copy()
+    for _ in range(int(np.ceil(np.log2(max(T, 2)))) + 1):
+        R = R | ((R.astype(np.int64) @ R.astype(np.int64)) > 0)
+    pad = np.array([p == W.PAD for p in parent])
+    depth = np.where(pad, -1, R.sum(1))
+    key = np.where(pad, T + 1, depth)
+    order = np.lexsort((np.arange(T), key))
+    return R, depth, order
+
+
+def test_golden_irregular_and_heap(orc):
+    cases, _ = _read_golden()
+    for name in ("irregular", "heap7"):
+        c = cases[name]
+        m = orc.prepare(np.array([c["parent"]], np.int32))
+        assert m["status"][0] == c["status"][0], name
+        assert m["nvalid"][0] == c["nvalid"][0], name
+        assert m["depth"][0].tolist() == c["depth"], name
+        assert m["order"][0].tolist() == c["order"], name
+        assert m["anc"][0, :, 0].astype(np.uint64).tolist() == c["anc"], name
+
+
+def test_golden_chain_word_boundary(orc):
+    cases, _ = _read_golden()
+    m = orc.prepare(W.chain_tree(70)[None])
+    assert m["anc"].shape == (1, 70, 2)
+    for node, depth, words in cases["chain70"]["checks"]:
+        assert m["depth"][0, node] == depth
+        assert [int(x) for x in m["anc"][0, node]] == words
+
+
+def test_golden_invalid_status(orc):
+    _, invalid = _read_golden()
+    assert len(invalid) >= 8
+    for st, arr in invalid:
+        m = orc.prepare(np.array([arr], np.int32))
+        assert m["status"][0] == st, arr
+        assert orc.tree_status(np.array(arr, np.int32)) == st
+        if st != 0:
+            # invalid sequences: depth -1, identity order, no ancestors, nvalid 0
+            assert (m["depth"][0] == -1).all()
+            assert m["order"][0].tolist() == list(range(len(arr)))
+            assert (m["anc"] == 0).all() and m["nvalid"][0] == 0
+
+
+@pytest.mark.parametrize("T", [1, 2, 7, 31, 64, 65, 128, 200])
+def test_closed_forms_heap_and_chain(orc, T):
+    m = orc.prepare(np.stack([W.heap_tree(T), W.chain_tree(T)]))
+    assert (m["status"] == 0).all() and (m["nvalid"] == T).all()
+    i = np.arange(T)
+    assert m["depth"][0].tolist() == np.floor(np.log2(i + 1)).astype(int).tolist()
+    assert m["depth"][1].tolist() == i.tolist()
+    assert m["order"][0].tolist() == i.tolist() and m["order"][1].tolist() == i.tolist()
+    Wd = (T + 63) // 64
+    for node in range(T):
+        # heap: ancestors are floor((node+1)/2^s) - 1, s = 1..depth
+        want = set()
+        s = 1
+        while (node + 1) >> s:
+            want.add(((node + 1) >> s) - 1)
+            s += 1
+        got = {j for j in range(T) if (int(m["anc"][0, node, j // 64]) >> (j % 64)) & 1}
+        assert got == want
+        # chain: {0..node-1}
+        got = {j for j in range(T) if (int(m["anc"][1, node, j // 64]) >> (j % 64)) & 1}
+        assert got == set(range(node))
+    assert m["anc"].shape == (2, T, Wd)
+
+
+def test_star(orc):
+    T = 50
+    p = np.zeros(T, np.int32)
+    p[0] = -1
+    m = orc.prepare(p[None])
+    assert m["depth"][0].tolist() == [0] + [1] * (T - 1)
+    assert all(int(m["anc"][0, i, 0]) == 1 for i in range(1, T))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_brute_force_random_trees(orc, seed):
+    rng = np.random.default_rng(seed)
+    T = int(rng.integers(1, 140))
+    nv = int(rng.integers(0, T + 1))
+    par = W.random_tree(rng, T, nv, shuffle=True)
+    m = orc.prepare(par[None])
+    assert m["status"][0] == 0 and m["nvalid"][0] == nv
+    R, depth, order = _closure_meta(par.tolist())
+    assert m["depth"][0].tolist() == depth.tolist()
+    assert m["order"][0].tolist() == order.tolist()
+    for i in range(T):
+        got = [bool((int(m["anc"][0, i, j // 64]) >> (j % 64)) & 1) for j in range(T)]
+        assert got == R[i].tolist()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_relabelling_invariance(orc, seed):
+    rng = np.random.default_rng(100 + seed)
+    T = 40
+    par = W.random_tree(rng, T, 33, shuffle=False)
+    perm = rng.permutation(T)
+    par2 = np.full(T, W.PAD, np.int32)
+    for i in range(T):
+        par2[perm[i]] = par[i] if par[i] < 0 else perm[par[i]]
+    m1, m2 = orc.prepare(par[None]), orc.prepare(par2[None])
+    for i in range(T):
+        assert m2["depth"][0, perm[i]] == m1["depth"][0, i]
+        a1 = {j for j in range(T) if (int(m1["anc"][0, i, 0]) >> j) & 1}
+        a2 = {j for j in range(T) if (int(m2["anc"][0, perm[i], 0]) >> j) & 1}
+        assert a2 == {int(perm[j]) for j in a1}
+    # canonical order: sorted by (depth, index) in either labelling
+    d2 = m2["depth"][0]
+    o2 = m2["order"][0]
+    keys = [(d2[n] if d2[n] >= 0 else T + 1, n) for n in o2]
+    assert keys == sorted(keys)
+
+
+def test_named_workload_trees(orc):
+    for cfg in range(5):
+        w = W.make_config(cfg)
+        m = orc.prepare(w.parent)
+        assert (m["status"] == 0).all() and (m["nvalid"] == w.T).all()
+        if cfg == 2:
+            assert m["depth"].max() == 8
+        if cfg == 4:
+            assert (m["depth"].max(axis=1) == 16).all()
+            for b in range(w.B):
+                assert np.bincount(w.parent[b][w.parent[b] >= 0]).max() <= 8
