@@ -1,0 +1,156 @@
+/*
+ * gdn_tree.h -- C ABI of libgdntree: rollback-free verification of a draft
+ * token tree through one Gated DeltaNet (GDN) layer on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * Method: "Trees from Marginals", Sec. 3.4.  Every tree node's output is the
+ * gated delta rule (Eq. 7) applied along that node's own root-to-node path,
+ * starting from the cached per-sequence state S0, followed by the readout of
+ * Eq. 8.  Verification never writes the cache; once the accepted node is
+ * known, a separate commit replays Eq. 7 along its path and writes the state
+ * (Sec. 3.4.2: "the only state write").  The tree metadata (depths, a
+ * topological order, proper-ancestor bitmasks) is computed once per decode
+ * step from parent pointers and shared by every GDN layer (Sec. 3.4.2).
+ *
+ * Conventions shared by all entry points
+ * --------------------------------------
+ *  * All tensor pointers are DEVICE pointers, contiguous row-major, owned by
+ *    the caller.  The library never allocates, frees or synchronises; work is
+ *    enqueued on the caller's stream and is ordered with it.  Pointers must be
+ *    16-byte aligned.
+ *  * Recurrence orientation: the stored state of (sequence b, value head h) is
+ *    S[b][h] in R^{dv x dk} (dk contiguous), the transpose of the paper's
+ *    S in R^{dk x dv}; one step is S <- alpha S (I - beta k k^T) + beta v k^T
+ *    and the readout is o = scale * S q (Eq. 7-8).
+ *  * Short convolution (width 4, depthwise, no bias) and activation: the raw
+ *    inputs of node t are the C = 2 Hk dk + Hv dv channels
+ *    x_t = [q_t (Hk heads) | k_t (Hk heads) | v_t (Hv heads)].  For a node i
+ *    at depth d with path p_0 = root, ..., p_d = i:
+ *        y_i[c] = SiLU( sum_{w=0..3} conv_w[c][w] * x_{p_{d-3+w}}[c] ),
+ *    where a tap above the root (d-3+w < 0) reads conv_state[b][d+w][c]
+ *    (slot 2 = most recent committed token, slot 0 = oldest).  q and k are
+ *    then L2-normalised per head: x / sqrt(sum x^2 + 1e-6).  v is not.
+ *  * GQA: value head h reads key head floor(h * Hk / Hv); Hv % Hk == 0.
+ *  * alpha (decay) and beta (write strength) are per value head, in (0, 1].
+ *  * Trees: parent[b][i] = -1 for the root, -2 for an absent (padding) slot,
+ *    else the parent's slot index.  Node numbering is arbitrary.
+ *
+ * Errors: every entry point returns gdn_status.  Problems visible on the
+ * host (null pointers, unsupported sizes) return an error before any work is
+ * enqueued; gdn_last_error() then describes it.  Problems that only the
+ * device can see (an invalid tree, an invalid accepted node) are reported per
+ * sequence in the status arrays below and the affected sequence is skipped.
+ */
+#ifndef GDN_TREE_H
+#define GDN_TREE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GDN_OK = 0,
+  GDN_EINVAL = -1,       /* null pointer, negative or inconsistent size */
+  GDN_EUNSUPPORTED = -2, /* valid but unsupported shape (head dims, T)   */
+  GDN_EHIP = -3          /* a HIP launch or attribute call failed        */
+} gdn_status;
+
+typedef enum { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
+
+/* Per-sequence status codes written by prepare (tree) and commit. */
+enum {
+  GDN_TREE_OK = 0,
+  GDN_TREE_NO_ROOT = 1,      /* real nodes but none with parent -1              */
+  GDN_TREE_MULTI_ROOT = 2,   /* more than one node with parent -1              */
+  GDN_TREE_BAD_PARENT = 3,   /* parent outside {-2,-1,0..T-1}, self, or padding */
+  GDN_TREE_CYCLE = 4,        /* a real node whose parent chain misses the root */
+  GDN_TREE_BAD_ACCEPTED = 5  /* commit only: accepted outside [-1,T) or padding */
+};
+
+/* Problem sizes.  B sequences, T node slots per tree (padded tree size),
+ * Hk key heads, Hv value heads, head dims dk and dv.
+ * in_dtype is the element type of q, k, v, alpha and beta (GDN_F32 or
+ * GDN_BF16); the state, conv weights, conv state and outputs are fp32.
+ * scale multiplies the readout; 0 selects 1/sqrt(dk) (Eq. 8).
+ * Supported: dk, dv in {16, 32, 64, 128}; 1 <= T <= GDN_MAX_T; B >= 0. */
+typedef struct {
+  int32_t B, T, Hk, Hv, dk, dv;
+  int32_t in_dtype;
+  float scale;
+} gdn_dims;
+
+#define GDN_MAX_T 128
+
+/* Size in bytes of the tree-metadata blob for B trees of T slots (host only,
+ * no device work).  Layout, W = ceil(T/64), all offsets multiples of 8:
+ *   uint64 anc   [B][T][W]  bit (j mod 64) of word j/64 of anc[b][i] is set
+ *                           iff slot j is a proper ancestor of slot i
+ *                           (Sec. 3.4.2 bitmask, node-index space)
+ *   int32  depth [B][T]     edges to the root; -1 for padding
+ *   int32  order [B][T]     canonical topological order: real nodes sorted
+ *                           by (depth, index), then padding by index
+ *   int32  pos   [B][T]     inverse permutation of order
+ *   int32  parent[B][T]     copy of the input parent array
+ *   int32  status[B]        GDN_TREE_* code of each tree
+ *   int32  nvalid[B]        number of real (non-padding) nodes
+ * A tree with a non-zero status gets depth -1, identity order/pos, empty
+ * ancestor sets and nvalid 0.  Returns 0 for B <= 0 or T <= 0. */
+size_t gdn_tree_meta_bytes(int32_t B, int32_t T);
+
+/* Tree preprocessing (Sec. 3.4.1 topological order and ancestor relation,
+ * Sec. 3.4.2 metadata computed once per decode step).
+ *   parent      int32 [B][T]   device, read-only
+ *   meta        device buffer of gdn_tree_meta_bytes(B, T) bytes, written
+ *   tree_status int32 [B]      device, written (may be NULL)
+ * Reads only dims->B and dims->T.  One workgroup per tree. */
+int gdn_tree_prepare(const gdn_dims* dims, const int32_t* parent, void* meta,
+                     int32_t* tree_status, hipStream_t stream);
+
+/* Read-only tree verification (Sec. 3.4: Eq. 7-8 per node along its path).
+ *   meta        written by gdn_tree_prepare for the same B, T
+ *   q, k        in_dtype [B][T][Hk][dk]   raw (pre-conv) queries / keys
+ *   v           in_dtype [B][T][Hv][dv]   raw values
+ *   alpha, beta in_dtype [B][T][Hv]
+ *   conv_w      fp32 [C][4]               C = 2 Hk dk + Hv dv
+ *   conv_state  fp32 [B][3][C]            read-only
+ *   S0          fp32 [B][Hv][dv][dk]      read-only cached state
+ *   out         fp32 [B][T][Hv][dv]       written: o_i = scale * S_i q_i
+ * Rows of padding slots and every row of a sequence whose tree status is
+ * non-zero are written as zeros.  conv_state and S0 are never written. */
+int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const void* k,
+                    const void* v, const void* alpha, const void* beta, const float* conv_w,
+                    const float* conv_state, const float* S0, float* out, hipStream_t stream);
+
+/* Commit of the accepted node (Sec. 3.4.2: a single pass replays Eq. 7 along
+ * the accepted path and writes the state).
+ *   accepted      int32 [B]  accepted slot per sequence, -1 = commit nothing
+ *   q, k, v, alpha, beta, conv_w: as for verify (same step's tensors)
+ *   conv_state    fp32 [B][3][C]   in/out: replaced by the last 3 raw inputs
+ *                 of (old slots 0..2 followed by the path's raw inputs)
+ *   S             fp32 [B][Hv][dv][dk]  in/out: state after the path
+ *   commit_status int32 [B] (may be NULL): the tree status if non-zero, else
+ *                 GDN_TREE_BAD_ACCEPTED for an accepted slot outside [-1, T)
+ *                 or naming padding, else 0.
+ * Sequences with accepted == -1 or a non-zero commit status are untouched.
+ * Enqueues two kernels (state replay, then conv-state shift). */
+int gdn_tree_commit(const gdn_dims* dims, const void* meta, const int32_t* accepted,
+                    const void* q, const void* k, const void* v, const void* alpha,
+                    const void* beta, const float* conv_w, float* conv_state, float* S,
+                    int32_t* commit_status, hipStream_t stream);
+
+/* Message describing the last non-OK return on the calling thread. */
+const char* gdn_last_error(void);
+
+/* Library version string. */
+const char* gdn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_TREE_H */

@@ -1,0 +1,131 @@
+// gdn_abi.hip -- the extern "C" boundary of libgdntree (declared in
+// include/gdn_tree.h): argument validation on the host, dispatch to the
+// templated kernel launchers, and the thread-local error message.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "gdn_internal.h"
+
+namespace gdn {
+
+static thread_local char g_err[512] = "";
+
+int set_error(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+static bool head_dim_ok(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }
+
+// Shape checks shared by verify and commit.
+static int check_dims(const gdn_dims* d, const char* who) {
+  if (!d) return set_error(GDN_EINVAL, "%s: dims is NULL", who);
+  if (d->B < 0 || d->T < 0 || d->Hk < 1 || d->Hv < 1)
+    return set_error(GDN_EINVAL, "%s: bad sizes B=%d T=%d Hk=%d Hv=%d", who, d->B, d->T, d->Hk,
+                     d->Hv);
+  if (d->Hv % d->Hk != 0)
+    return set_error(GDN_EINVAL, "%s: Hv=%d is not a multiple of Hk=%d", who, d->Hv, d->Hk);
+  if (d->in_dtype != GDN_F32 && d->in_dtype != GDN_BF16)
+    return set_error(GDN_EINVAL, "%s: in_dtype=%d", who, d->in_dtype);
+  if (!(d->scale >= 0.0f) || isinf(d->scale))
+    return set_error(GDN_EINVAL, "%s: scale must be finite and >= 0", who);
+  if (!head_dim_ok(d->dk) || !head_dim_ok(d->dv))
+    return set_error(GDN_EUNSUPPORTED, "%s: dk=%d dv=%d (supported 16, 32, 64, 128)", who, d->dk,
+                     d->dv);
+  if (d->T > GDN_MAX_T) return set_error(GDN_EUNSUPPORTED, "%s: T=%d > %d", who, d->T, GDN_MAX_T);
+  return GDN_OK;
+}
+
+}  // namespace gdn
+
+using namespace gdn;
+
+extern "C" {
+
+size_t gdn_tree_meta_bytes(int32_t B, int32_t T) {
+  if (B <= 0 || T <= 0) return 0;
+  return meta_layout(B, T).total;
+}
+
+int gdn_tree_prepare(const gdn_dims* dims, const int32_t* parent, void* meta,
+                     int32_t* tree_status, hipStream_t stream) {
+  if (!dims) return set_error(GDN_EINVAL, "prepare: dims is NULL");
+  if (dims->B < 0 || dims->T < 0)
+    return set_error(GDN_EINVAL, "prepare: bad sizes B=%d T=%d", dims->B, dims->T);
+  if (dims->T > GDN_MAX_T)
+    return set_error(GDN_EUNSUPPORTED, "prepare: T=%d > %d", dims->T, GDN_MAX_T);
+  if (dims->B == 0 || dims->T == 0) return GDN_OK;
+  if (!parent || !meta) return set_error(GDN_EINVAL, "prepare: NULL parent or meta");
+  return launch_prepare(dims->B, dims->T, parent, meta, tree_status, stream);
+}
+
+int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const void* k,
+                    const void* v, const void* alpha, const void* beta, const float* conv_w,
+                    const float* conv_state, const float* S0, float* out, hipStream_t stream) {
+  int rc = check_dims(dims, "verify");
+  if (rc != GDN_OK) return rc;
+  if (dims->B == 0 || dims->T == 0) return GDN_OK;
+  if (!meta || !q || !k || !v || !alpha || !beta || !conv_w || !conv_state || !S0 || !out)
+    return set_error(GDN_EINVAL, "verify: NULL tensor pointer");
+  VerifyArgs a;
+  a.B = dims->B;
+  a.T = dims->T;
+  a.Hk = dims->Hk;
+  a.Hv = dims->Hv;
+  a.dk = dims->dk;
+  a.dv = dims->dv;
+  a.in_dtype = dims->in_dtype;
+  a.scale = dims->scale > 0.0f ? dims->scale : 1.0f / sqrtf(float(dims->dk));
+  a.meta = meta;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.conv_w = conv_w;
+  a.conv_state = conv_state;
+  a.S0 = S0;
+  a.out = out;
+  return launch_verify(a, stream);
+}
+
+int gdn_tree_commit(const gdn_dims* dims, const void* meta, const int32_t* accepted,
+                    const void* q, const void* k, const void* v, const void* alpha,
+                    const void* beta, const float* conv_w, float* conv_state, float* S,
+                    int32_t* commit_status, hipStream_t stream) {
+  int rc = check_dims(dims, "commit");
+  if (rc != GDN_OK) return rc;
+  if (dims->B == 0 || dims->T == 0) return GDN_OK;
+  if (!meta || !accepted || !q || !k || !v || !alpha || !beta || !conv_w || !conv_state || !S)
+    return set_error(GDN_EINVAL, "commit: NULL tensor pointer");
+  CommitArgs a;
+  a.B = dims->B;
+  a.T = dims->T;
+  a.Hk = dims->Hk;
+  a.Hv = dims->Hv;
+  a.dk = dims->dk;
+  a.dv = dims->dv;
+  a.in_dtype = dims->in_dtype;
+  a.meta = meta;
+  a.accepted = accepted;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.conv_w = conv_w;
+  a.conv_state = conv_state;
+  a.S = S;
+  a.commit_status = commit_status;
+  return launch_commit(a, stream);
+}
+
+const char* gdn_last_error(void) { return g_err; }
+
+const char* gdn_version(void) { return "gdntree 0.1 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+// gdn_internal.h -- private declarations of libgdntree (kernels + launchers).
+//
+// Device helpers used by the prepare / verify / commit kernels, the layout of
+// the tree-metadata blob and the launcher entry points that the C ABI
+// (gdn_abi.hip) dispatches to.  Everything here targets gfx950 (CDNA4,
+// wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gdn_tree.h"
+
+namespace gdn {
+
+constexpr int kWave = 64;
+constexpr int kPad = -2;   // parent value of an absent slot
+constexpr int kRoot = -1;  // parent value of the root
+
+// ---------------------------------------------------------------------------
+// Tree-metadata blob (layout documented in gdn_tree.h).  Each array starts at
+// a 16-byte aligned offset.
+// ---------------------------------------------------------------------------
+struct MetaLayout {
+  size_t anc, depth, order, pos, parent, status, nvalid, total;
+  int W;
+};
+
+__host__ __device__ inline size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
+
+__host__ __device__ inline MetaLayout meta_layout(int B, int T) {
+  MetaLayout m;
+  m.W = (T + 63) / 64;
+  size_t bt = size_t(B) * size_t(T);
+  m.anc = 0;
+  m.depth = align16(m.anc + 8 * bt * m.W);
+  m.order = align16(m.depth + 4 * bt);
+  m.pos = align16(m.order + 4 * bt);
+  m.parent = align16(m.pos + 4 * bt);
+  m.status = align16(m.parent + 4 * bt);
+  m.nvalid = align16(m.status + 4 * size_t(B));
+  size_t end = m.nvalid + 4 * size_t(B);
+  m.total = (end + 255) & ~size_t(255);
+  return m;
+}
+
+struct MetaPtrs {
+  uint64_t* anc;
+  int32_t* depth;
+  int32_t* order;
+  int32_t* pos;
+  int32_t* parent;
+  int32_t* status;
+  int32_t* nvalid;
+  int W;
+};
+
+__host__ __device__ inline MetaPtrs meta_ptrs(const void* base, int B, int T) {
+  MetaLayout l = meta_layout(B, T);
+  char* p = (char*)base;
+  MetaPtrs m;
+  m.anc = (uint64_t*)(p + l.anc);
+  m.depth = (int32_t*)(p + l.depth);
+  m.order = (int32_t*)(p + l.order);
+  m.pos = (int32_t*)(p + l.pos);
+  m.parent = (int32_t*)(p + l.parent);
+  m.status = (int32_t*)(p + l.status);
+  m.nvalid = (int32_t*)(p + l.nvalid);
+  m.W = l.W;
+  return m;
+}
+
+// ---------------------------------------------------------------------------
+// Element loads: inputs are fp32 or bf16 (stored as raw 16-bit patterns).
+// ---------------------------------------------------------------------------
+struct BF16 {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(BF16 x) {
+  return __uint_as_float(uint32_t(x.bits) << 16);
+}
+
+template <typename TIn>
+__device__ __forceinline__ float ld(const TIn* p, size_t i) {
+  return to_f32(p[i]);
+}
+
+// 4 consecutive elements starting at p (4-element aligned).
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4(const BF16* p) {
+  uint2 u = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+__device__ __forceinline__ float silu(float y) { return y / (1.0f + __expf(-y)); }
+
+// ---------------------------------------------------------------------------
+// Launchers (defined in the kernel sources).  All return a gdn_status value.
+// ---------------------------------------------------------------------------
+int launch_prepare(int B, int T, const int32_t* parent, void* meta, int32_t* tree_status,
+                   hipStream_t stream);
+
+struct VerifyArgs {
+  int B, T, Hk, Hv, dk, dv, in_dtype;
+  float scale;
+  const void* meta;
+  const void *q, *k, *v, *alpha, *beta;
+  const float *conv_w, *conv_state, *S0;
+  float* out;
+};
+int launch_verify(const VerifyArgs& a, hipStream_t stream);
+
+struct CommitArgs {
+  int B, T, Hk, Hv, dk, dv, in_dtype;
+  const void* meta;
+  const int32_t* accepted;
+  const void *q, *k, *v, *alpha, *beta;
+  const float* conv_w;
+  float* conv_state;
+  float* S;
+  int32_t* commit_status;
+};
+int launch_commit(const CommitArgs& a, hipStream_t stream);
+
+// Records a message for gdn_last_error() and returns code.
+int set_error(int code, const char* fmt, ...);
+
+}  // namespace gdn

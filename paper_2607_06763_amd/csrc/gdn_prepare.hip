@@ -1,0 +1,145 @@
+// gdn_prepare.hip -- tree preprocessing kernel (paper Sec. 3.4.1 ancestor
+// relation and topological order; Sec. 3.4.2 metadata computed once per
+// decode step from parent pointers: proper-ancestor sets as bitmasks packed
+// in 64-bit words).
+//
+// One workgroup per tree, one thread per slot (T <= kPrepMaxT).  Depth and
+// ancestor sets come from pointer jumping: after r rounds every slot knows
+// its ancestors at distances 1..2^r and the ancestor at distance 2^r, so
+// ceil(log2 T) rounds reach the root from any connected slot; a slot that
+// still has an ancestor to jump to afterwards lies on a cycle.  The
+// canonical order ranks slots by (depth, index) with padding last.
+#include "gdn_internal.h"
+
+namespace gdn {
+
+constexpr int kPrepMaxT = 512;
+constexpr int kPrepMaxW = kPrepMaxT / 64;
+
+__global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __restrict__ parent,
+                                                            MetaPtrs m, int32_t* tree_status,
+                                                            int T) {
+  __shared__ int s_par[kPrepMaxT];
+  __shared__ int s_nxt[kPrepMaxT];
+  __shared__ int s_dep[kPrepMaxT];
+  __shared__ uint64_t s_anc[kPrepMaxT * kPrepMaxW];
+  __shared__ int s_bad, s_roots, s_real, s_cycle;
+
+  const int b = blockIdx.x;
+  const int i = threadIdx.x;
+  const int W = m.W;
+  const bool slot = i < T;
+
+  if (i == 0) {
+    s_bad = 0;
+    s_roots = 0;
+    s_real = 0;
+    s_cycle = 0;
+  }
+  int p = slot ? parent[size_t(b) * T + i] : kPad;
+  if (slot) s_par[i] = p;
+  __syncthreads();
+
+  // validity of the parent value itself
+  const bool real = slot && p != kPad;
+  if (real) {
+    atomicAdd(&s_real, 1);
+    if (p == kRoot) {
+      atomicAdd(&s_roots, 1);
+    } else if (p < 0 || p >= T || p == i || s_par[p] == kPad) {
+      s_bad = 1;
+    }
+  }
+  __syncthreads();
+  int status = GDN_TREE_OK;
+  if (s_bad)
+    status = GDN_TREE_BAD_PARENT;
+  else if (s_real > 0 && s_roots == 0)
+    status = GDN_TREE_NO_ROOT;
+  else if (s_roots > 1)
+    status = GDN_TREE_MULTI_ROOT;
+
+  // pointer jumping (only meaningful for a tree with valid parent values)
+  uint64_t anc[kPrepMaxW];
+#pragma unroll
+  for (int w = 0; w < kPrepMaxW; ++w) anc[w] = 0;
+  int nxt = (real && p >= 0 && status == GDN_TREE_OK) ? p : -1;
+  int dep = (nxt >= 0) ? 1 : 0;
+#pragma unroll
+  for (int w = 0; w < kPrepMaxW; ++w)
+    if (nxt >= 0 && w == (nxt >> 6)) anc[w] |= 1ull << (nxt & 63);
+  for (int span = 1; span < T; span <<= 1) {
+    if (slot) {
+      s_nxt[i] = nxt;
+      s_dep[i] = dep;
+#pragma unroll
+      for (int w = 0; w < kPrepMaxW; ++w)
+        if (w < W) s_anc[i * kPrepMaxW + w] = anc[w];
+    }
+    __syncthreads();
+    if (nxt >= 0) {
+      int j = nxt;
+      dep += s_dep[j];
+#pragma unroll
+      for (int w = 0; w < kPrepMaxW; ++w)
+        if (w < W) anc[w] |= s_anc[j * kPrepMaxW + w];
+      nxt = s_nxt[j];
+    }
+    __syncthreads();
+  }
+  if (status == GDN_TREE_OK && real && nxt >= 0) s_cycle = 1;
+  __syncthreads();
+  if (status == GDN_TREE_OK && s_cycle) status = GDN_TREE_CYCLE;
+
+  const int32_t base = b * T;
+  if (status != GDN_TREE_OK) {
+    if (slot) {
+      m.depth[base + i] = -1;
+      m.order[base + i] = i;
+      m.pos[base + i] = i;
+      m.parent[base + i] = p;
+      for (int w = 0; w < W; ++w) m.anc[(size_t(base) + i) * W + w] = 0;
+    }
+    if (i == 0) {
+      m.status[b] = status;
+      m.nvalid[b] = 0;
+      if (tree_status) tree_status[b] = status;
+    }
+    return;
+  }
+
+  // canonical order: rank by key (depth, index); padding keyed after all depths
+  if (slot) s_dep[i] = real ? dep : T + 1;
+  __syncthreads();
+  if (slot) {
+    const int key = s_dep[i];
+    int rank = 0;
+    for (int j = 0; j < T; ++j) {
+      int kj = s_dep[j];
+      rank += (kj < key) || (kj == key && j < i);
+    }
+    m.order[base + rank] = i;
+    m.pos[base + i] = rank;
+    m.depth[base + i] = real ? dep : -1;
+    m.parent[base + i] = p;
+    for (int w = 0; w < W; ++w) m.anc[(size_t(base) + i) * W + w] = real ? anc[w] : 0;
+  }
+  if (i == 0) {
+    m.status[b] = GDN_TREE_OK;
+    m.nvalid[b] = s_real;
+    if (tree_status) tree_status[b] = GDN_TREE_OK;
+  }
+}
+
+int launch_prepare(int B, int T, const int32_t* parent, void* meta, int32_t* tree_status,
+                   hipStream_t stream) {
+  if (T > kPrepMaxT) return set_error(GDN_EUNSUPPORTED, "prepare: T=%d exceeds %d", T, kPrepMaxT);
+  MetaPtrs m = meta_ptrs(meta, B, T);
+  int threads = ((T + kWave - 1) / kWave) * kWave;
+  hipLaunchKernelGGL(prepare_kernel, dim3(B), dim3(threads), 0, stream, parent, m, tree_status, T);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(GDN_EHIP, "prepare launch: %s", hipGetErrorString(e));
+  return GDN_OK;
+}
+
+}  // namespace gdn

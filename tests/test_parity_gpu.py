@@ -1,0 +1,287 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: tree metadata, statuses and the conv state are bit-exact; verify
+outputs satisfy max|o - o_ref| <= 2e-3 * max|o_ref|; the committed fp32
+state satisfies ||S - S_ref||_F <= 1e-4 ||S_ref||_F for every
+(sequence, value head).  The large workload (32 x 128-node trees, 48 value
+heads) is checked on sampled nodes, which the oracle evaluates one by one.
+"""
+import numpy as np
+import pytest
+
+from paper_2607_06763_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-3
+S_TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_06763_amd import gdn_tree as G
+    G.lib()
+    return G
+
+
+def _announce(msg):
+    print(f"[gpu] {msg}", flush=True)
+
+
+def _check_meta(G, dt, w, orc):
+    ref = orc.prepare(w.parent)
+    got = dt.meta_arrays()
+    for key in ("depth", "order", "anc", "nvalid", "status"):
+        np.testing.assert_array_equal(got[key], ref[key], err_msg=key)
+    ok = ref["status"] == 0
+    if ok.any():
+        pos = np.argsort(ref["order"], axis=1)
+        np.testing.assert_array_equal(got["pos"][ok], pos[ok])
+    np.testing.assert_array_equal(got["parent"], w.parent)
+    np.testing.assert_array_equal(dt.tree_status.cpu().numpy(), ref["status"])
+
+
+def _run_verify(G, w, dt=None):
+    import torch
+    dt = dt or G.DeviceTree(w)
+    dt.prepare()
+    dt.verify()
+    torch.cuda.synchronize()
+    return dt, dt.out.cpu().numpy().astype(np.float64)
+
+
+def _out_err(got, ref):
+    scale = max(np.max(np.abs(ref)), 1e-30)
+    return np.max(np.abs(got - ref)) / scale
+
+
+def _state_err(S_got, S_ref):
+    B, H = S_ref.shape[:2]
+    num = np.sqrt(np.sum((S_got.astype(np.float64) - S_ref) ** 2, axis=(2, 3)))
+    den = np.sqrt(np.sum(S_ref ** 2, axis=(2, 3)))
+    return np.max(num / np.maximum(den, 1e-30))
+
+
+def _sample_mask(w, per_seq, seed):
+    rng = np.random.default_rng(seed)
+    mask = np.zeros((w.B, w.T), np.uint8)
+    for b in range(w.B):
+        real = np.nonzero(w.parent[b] != W.PAD)[0]
+        depth = np.zeros(w.T, int)
+        for i in range(w.T):  # parent[i] < i in the named workloads
+            p = w.parent[b, i]
+            depth[i] = 0 if p < 0 else depth[p] + 1
+        pick = {int(w.accepted[b]), int(real[np.argmax(depth[real])]), int(real[0])}
+        pick |= set(int(x) for x in rng.choice(real, size=min(per_seq, len(real)), replace=False))
+        mask[b, sorted(pick)] = 1
+    return mask
+
+
+# ---------------------------------------------------------------------------
+# named workloads
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_prepare_bit_exact(G, orc, cfg):
+    w = W.make_config(cfg)
+    _announce(f"prepare cfg={cfg} B={w.B} T={w.T}")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    _check_meta(G, dt, w, orc)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_verify_named_full(G, orc, cfg):
+    w = W.make_config(cfg)
+    _announce(f"verify cfg={cfg} B={w.B} T={w.T} Hk={w.Hk} Hv={w.Hv} d={w.dk}")
+    _dt, got = _run_verify(G, w)
+    ref = orc.verify(w)
+    err = _out_err(got, ref)
+    _announce(f"  max|err|/max|ref| = {err:.3e}")
+    assert err <= O_TOL
+
+
+def test_verify_large_sampled(G, orc):
+    w = W.make_config(4)
+    _announce(f"verify cfg=4 B={w.B} T={w.T} Hv={w.Hv} (sampled)")
+    _dt, got = _run_verify(G, w)
+    mask = _sample_mask(w, 2, 7)
+    ref = orc.verify(w, node_mask=mask)
+    sel = mask.astype(bool)
+    err = _out_err(got[sel], ref[sel])
+    _announce(f"  {sel.sum()} nodes, max|err|/max|ref| = {err:.3e}")
+    assert err <= O_TOL
+    assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_commit_named(G, orc, cfg):
+    import torch
+    w = W.make_config(cfg)
+    _announce(f"commit cfg={cfg}")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    S_ref, cs_ref, st_ref = orc.commit(w)
+    np.testing.assert_array_equal(dt.commit_status.cpu().numpy(), st_ref)
+    err = _state_err(S.cpu().numpy(), S_ref)
+    _announce(f"  max per-head rel Frobenius = {err:.3e}")
+    assert err <= S_TOL
+    np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))
+
+
+def test_verify_is_read_only_and_deterministic(G):
+    import torch
+    w = W.make_config(3)
+    dt = G.DeviceTree(w)
+    S0_before = dt.S0.clone()
+    cs_before = dt.conv_state.clone()
+    dt.prepare()
+    dt.verify()
+    o1 = dt.out.clone()
+    dt.verify()
+    torch.cuda.synchronize()
+    assert torch.equal(dt.S0.view(torch.int32), S0_before.view(torch.int32))
+    assert torch.equal(dt.conv_state.view(torch.int32), cs_before.view(torch.int32))
+    assert torch.equal(o1.view(torch.int32), dt.out.view(torch.int32))
+
+
+# ---------------------------------------------------------------------------
+# random shapes, padding, relabelling
+# ---------------------------------------------------------------------------
+SHAPES = [
+    # (B, T, Hk, Hv, dk, dv, dtype, n_valid per seq or None, max_depth)
+    (2, 1, 1, 1, 16, 16, "f32", None, None),
+    (3, 9, 2, 6, 32, 16, "bf16", [9, 5, 1], None),
+    (2, 33, 1, 3, 64, 128, "bf16", [33, 20], 4),
+    (1, 64, 2, 4, 128, 32, "f32", None, None),
+    (2, 100, 3, 3, 16, 64, "bf16", [100, 71], 12),
+    (2, 128, 1, 2, 128, 128, "bf16", [128, 97], None),
+    (1, 128, 1, 1, 32, 32, "f32", None, None),   # deep random tree
+    (4, 17, 4, 8, 64, 64, "bf16", [17, 0, 3, 16], 3),  # includes an empty tree
+]
+
+
+@pytest.mark.parametrize("idx", range(len(SHAPES)))
+def test_random_shapes_verify_commit(G, orc, idx):
+    import torch
+    B, T, Hk, Hv, dk, dv, dt_, nv, md = SHAPES[idx]
+    w = W.make_random(1000 + idx, B, T, Hk, Hv, dk, dv, dt_, n_valid=nv, shuffle=True,
+                      max_depth=md)
+    _announce(f"random shape {SHAPES[idx]}")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    _check_meta(G, dt, w, orc)
+    dt.verify()
+    torch.cuda.synchronize()
+    got = dt.out.cpu().numpy().astype(np.float64)
+    ref = orc.verify(w)
+    err = _out_err(got, ref)
+    _announce(f"  verify err {err:.3e}")
+    assert err <= O_TOL
+    pad = w.parent == W.PAD
+    assert (got[pad] == 0).all()
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    S_ref, cs_ref, st_ref = orc.commit(w)
+    np.testing.assert_array_equal(dt.commit_status.cpu().numpy(), st_ref)
+    assert _state_err(S.cpu().numpy(), S_ref) <= S_TOL
+    np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))
+
+
+def test_chain_deep_and_custom_scale(G, orc):
+    import torch
+    w = W.make_random(2000, 1, 128, 2, 4, 64, 32, "bf16", parent=W.chain_tree(128)[None])
+    dt = G.DeviceTree(w, scale=0.25)
+    dt.prepare()
+    dt.verify()
+    torch.cuda.synchronize()
+    err = _out_err(dt.out.cpu().numpy(), orc.verify(w, scale=0.25))
+    assert err <= O_TOL
+
+
+def test_invalid_trees(G, orc):
+    import torch
+    T = 8
+    par = np.array([
+        [-1, 0, 0, 1, 1, 2, 2, 3],      # ok
+        [-1, 0, 9, 1, 1, 2, 2, 3],      # out of range
+        [1, 0, -2, -2, -2, -2, -2, -2],  # no root
+        [-1, -1, 0, 1, -2, -2, -2, -2],  # two roots
+        [-1, 2, 1, 0, -2, -2, -2, -2],  # cycle
+        [-1, 0, -2, 2, -2, -2, -2, -2],  # parent is padding
+        [-2] * 8,                       # empty
+    ], np.int32)
+    w = W.make_random(3000, par.shape[0], T, 2, 2, 16, 32, "bf16", parent=par)
+    w.accepted[:] = [3, 0, 0, 0, 0, 0, -1]
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    _check_meta(G, dt, w, orc)
+    dt.verify()
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    got = dt.out.cpu().numpy()
+    ref = orc.verify(w)
+    assert _out_err(got, ref) <= O_TOL
+    assert (got[1:] == 0).all()
+    S_ref, cs_ref, st_ref = orc.commit(w)
+    np.testing.assert_array_equal(dt.commit_status.cpu().numpy(), st_ref)
+    assert st_ref.tolist() == [0, 3, 1, 2, 4, 3, 0]
+    assert torch.equal(S[1:], dt.S0[1:])
+    assert _state_err(S.cpu().numpy(), S_ref) <= S_TOL
+    np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))
+
+
+def test_bad_accepted(G, orc):
+    import torch
+    par = np.stack([W.chain_tree(6)] * 4)
+    par[3, 5] = W.PAD
+    w = W.make_random(3100, 4, 6, 1, 2, 32, 16, "f32", parent=par)
+    w.accepted[:] = [-1, 6, -5, 5]   # skip, out of range, out of range, padding
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    assert dt.commit_status.cpu().numpy().tolist() == [0, 5, 5, 5]
+    assert torch.equal(S, dt.S0) and torch.equal(cs, dt.conv_state)
+
+
+def test_multi_step_resume(G, orc):
+    """Three decode steps of (prepare, verify, commit) with fresh trees each step:
+    the device state and conv state after every commit match the oracle chained
+    through the same steps, and so does every step's verify."""
+    import torch
+    S = cs = S_ref = cs_ref = conv_w = None
+    for step in range(3):
+        w = W.make_random(4000 + step, 3, 40, 2, 4, 64, 64, "bf16", shuffle=True)
+        conv_w = w.conv_w.copy() if conv_w is None else conv_w
+        w.conv_w = conv_w                      # one layer: same weights every step
+        dt = G.DeviceTree(w)
+        if S is None:
+            S, cs = dt.S0.clone(), dt.conv_state.clone()
+            S_ref, cs_ref = w.S0.astype(np.float64), w.conv_state.astype(np.float64)
+        w.S0 = S_ref
+        w.conv_state = cs_ref
+        dt.prepare()
+        dt.verify(S0=S, conv_state=cs)
+        dt.commit(S, cs)
+        torch.cuda.synchronize()
+        ref_out = orc.verify(w)
+        assert _out_err(dt.out.cpu().numpy(), ref_out) <= O_TOL
+        S_ref, cs_ref, st = orc.commit(w)
+        assert _state_err(S.cpu().numpy(), S_ref) <= S_TOL
+        np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))
+        # keep the oracle on the device's fp32 state so errors do not compound
+        S_ref = S.cpu().numpy().astype(np.float64)
+        cs_ref = cs.cpu().numpy().astype(np.float64)
