@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark of rollback-free GDN draft-tree verification on one MI355X.
+
+One step = one pass of the whole hot path for one GDN layer over one batch of
+synthetic draft trees: tree prepare, verify (every node's output from the
+read-only cached state) and commit (state + conv state of the accepted node).
+The default workload is the large one: 32 trees of 128 nodes (depth 16),
+16 key / 48 value heads, dk = dv = 128, bf16 inputs, fp32 state.
+
+Prints ONE JSON line on stdout: throughput in tree nodes verified per second
+per GDN layer, the roofline of the dominant kernel (verify), and the CPU
+oracle's throughput on the same workload.  Per-kernel durations come from HIP
+events recorded on the stream the kernels are launched on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+VERIFY_SOURCES = ("paper_2607_06763_amd/csrc/gdn_verify.hip", "paper_2607_06763_amd/csrc/gdn_internal.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "verify_large_hbm_traffic.md")
+
+
+def verify_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in VERIFY_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(w) -> dict:
+    """Bytes the method must move (each input read once, each output written
+    once), per launch of each kernel."""
+    import numpy as np
+    B, T, Hk, Hv, dk, dv = w.B, w.T, w.Hk, w.Hv, w.dk, w.dv
+    e = 2 if w.in_dtype == "bf16" else 4
+    C = 2 * Hk * dk + Hv * dv
+    meta_read = 4 * 4 * B * T + 8 * B            # order, depth, parent, pos + status, nvalid
+    verify = (4 * B * Hv * dv * dk                # S0
+              + e * B * T * (2 * Hk * dk + Hv * dv)  # q, k, v
+              + e * 2 * B * T * Hv                 # alpha, beta
+              + 4 * 3 * B * C + 4 * 4 * C          # conv state, conv weights
+              + meta_read
+              + 4 * B * T * Hv * dv)               # out
+    # commit: S read + write, conv state read + write, raw inputs and gates of
+    # the accepted paths, conv weights
+    depth = np.zeros((B, T), int)
+    for b in range(B):
+        for i in range(T):
+            p = w.parent[b, i]
+            depth[b, i] = 0 if p < 0 else depth[b, p] + 1
+    L = sum(depth[b, w.accepted[b]] + 1 for b in range(B) if w.accepted[b] >= 0)
+    commit = (2 * 4 * B * Hv * dv * dk + 2 * 4 * 3 * B * C + int(L) * (e * C + 2 * e * Hv)
+              + 4 * 4 * C + 8 * B * T + 8 * B)
+    prepare = 4 * B * T + 8 * B * T * ((T + 63) // 64) + 4 * 4 * B * T + 8 * B
+    return {"verify": int(verify), "commit": int(commit), "prepare": int(prepare)}
+
+
+def measured_traffic(src_hash: str):
+    """HBM bytes per verify launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if ":" in line and line.startswith("- "):
+                k, v = line[2:].split(":", 1)
+                vals[k.strip()] = v.strip().strip("`")
+    if vals.get("verify_source_sha256_16") != src_hash:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, max_seconds: float = 30.0) -> dict:
+    """The oracle (prepare + verify + commit) timed on this host's cores on
+    whole trees of the same workload; as many trees as fit the time budget,
+    estimated from the first tree."""
+    import copy
+
+    from oracle import oracle as orc
+
+    def sub(nb):
+        s = copy.copy(w)
+        s.B = nb
+        for n in ("parent", "q", "k", "v", "alpha", "beta", "S0", "conv_state", "accepted"):
+            setattr(s, n, getattr(w, n)[:nb])
+        return s
+
+    def run(s):
+        t0 = time.perf_counter()
+        orc.prepare(s.parent)
+        orc.verify(s)
+        orc.commit(s)
+        return time.perf_counter() - t0
+
+    t1 = run(sub(1))
+    nb = max(1, min(w.B, int(max_seconds / max(t1, 1e-6))))
+    s = sub(nb)
+    dt = run(s) if nb > 1 else t1
+    return {"value": round(nb * w.T / dt, 2), "unit": "nodes/s", "cores": orc.num_threads(),
+            "kind": "oracle",
+            "sample": f"{nb} of {w.B} trees x {w.T} nodes of the '{w.name}' workload, all "
+                      f"{w.Hv} value heads; prepare+verify+commit; fp64 per-node path replay; "
+                      f"{dt:.2f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=4, help="workload index 0..4 (default: large)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="after timing, run 5 plain device copies of this many MiB (a known-size "
+                         "kernel for scaling HBM counters)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): every "
+              "(sequence, head) unit is independent and this build has no multi-GPU path.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2607_06763_amd import gdn_tree as G
+    from paper_2607_06763_amd import workloads as W
+
+    if not os.path.exists(G.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    torch.cuda.set_device(0)
+    w = W.make_config(args.config)
+    dt = G.DeviceTree(w, device="cuda:0")
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    nbytes = algorithmic_bytes(w)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        dt.prepare()
+        if ev is not None:
+            ev[1].record()
+        dt.verify(S0=S, conv_state=cs)
+        if ev is not None:
+            ev[2].record()
+        dt.commit(S, cs)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                    for e in events]) * 1e3  # us
+    us_prep, us_ver, us_com = (float(x) for x in per.mean(0))
+    p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
+
+    nodes = w.B * w.T
+    ach = nbytes["verify"] / (us_ver * 1e-6) / 1e9
+    src_hash = verify_source_hash()
+    traffic = measured_traffic(src_hash)
+    roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "verify", "algorithmic_bytes_per_launch": nbytes["verify"],
+                "avg_launch_us": round(us_ver, 3)}
+    out = {
+        "metric": "tree nodes verified/s per GDN layer",
+        "value": round(nodes / (ms_step * 1e-3), 1),
+        "unit": "nodes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.B} trees x T={w.T} nodes, Hk={w.Hk} Hv={w.Hv} "
+                               f"dk={w.dk} dv={w.dv}, {w.in_dtype} inputs, fp32 state and output",
+                   "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+        "detail": {
+            "us_prepare": round(us_prep, 3), "us_verify": round(us_ver, 3),
+            "us_verify_p10_p50_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
+            "us_commit": round(us_com, 3),
+            "nodes_per_s_verify_only": round(nodes / (us_ver * 1e-6), 1),
+            "verify_hbm_frac": round(ach / HBM_PEAK_GBS, 4),
+            "commit_GBs": round(nbytes["commit"] / (us_com * 1e-6) / 1e9, 1),
+            "verify_plus_commit_hbm_frac": round(
+                (nbytes["verify"] + nbytes["commit"]) / ((us_ver + us_com) * 1e-6) / 1e9
+                / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes": nbytes,
+            "verify_source_sha256_16": src_hash,
+        },
+    }
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["detail"]["copy_calibration_bytes_each"] = 2 * 4 * n
+        del src, dst
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
