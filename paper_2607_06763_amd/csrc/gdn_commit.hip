@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kCT) void commit_state_kernel(CommitParams p) {
       }
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) ss += __shfl_xor(ss, o);
-      const float inv = 1.0f / sqrtf(ss + 1e-6f);
+      const float inv = rsqrt_hw(ss + 1e-6f);
 #pragma unroll
       for (int e = 0; e < KPL; ++e) {
         const int c = lane * KPL + e;

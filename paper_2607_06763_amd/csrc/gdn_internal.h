@@ -95,7 +95,14 @@ __device__ __forceinline__ float4 ld4(const BF16* p) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
 
-__device__ __forceinline__ float silu(float y) { return y / (1.0f + __expf(-y)); }
+// SiLU(y) = y * sigmoid(y) with the hardware exp2 and reciprocal (1 ulp each)
+// instead of an IEEE-exact division sequence.
+__device__ __forceinline__ float silu(float y) {
+  return y * __builtin_amdgcn_rcpf(1.0f + __expf(-y));
+}
+
+// 1 / sqrt(x) with the hardware reciprocal square root (1 ulp)
+__device__ __forceinline__ float rsqrt_hw(float x) { return __builtin_amdgcn_rsqf(x); }
 
 // ---------------------------------------------------------------------------
 // Launchers (defined in the kernel sources).  All return a gdn_status value.

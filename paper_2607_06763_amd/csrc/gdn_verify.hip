@@ -9,24 +9,33 @@
 // node.  In the stored orientation (S in R^{dv x dk}, o = scale S q), one
 // step gives S_t x = alpha_t S_{t-1} (x - beta_t (k_t.x) k_t) + beta_t (k_t.x) v_t
 // for any vector x, so walking i's path from the leaf to the root with
-//     x <- q_i, r <- 1;   for t = i, parent(i), ..., root:
-//         s = k_t.x;  c_t = r beta_t s;  x <- x - beta_t s k_t;  r <- r alpha_t
-// yields  o_i = scale * ( r S0 x + sum_t c_t v_t ),  r = a_i = prod alpha.
-// The leaf-to-root walk ("query pull-back") is O(depth * dk) vector work per
-// node; the rest is one dense product per (sequence, value head):
-//     O = scale * [ diag(a) X~ | C ] . [ S0^T ; V ]
-// with X~ the pulled-back queries (T x dk) and C the ancestor-masked
-// coefficients (T x T, lower triangular in the canonical order).  That
-// product runs on the MFMA units with a bf16 hi/lo split of both operands
-// (three bf16 products per tile, fp32 accumulation, ~1e-5 relative error).
+//     x <- q_i, r <- 1, acc <- 0;   for t = i, parent(i), ..., root:
+//         s = k_t.x;  acc += r beta_t s v_t;  x <- x - beta_t s k_t;  r <- r alpha_t
+// yields  o_i = scale * ( r S0 x + acc ),  r = a_i = prod of alpha on the path.
+// The leaf-to-root walk ("query pull-back") is O(depth (2 dk + dv)) vector
+// work per node on the VALU; the one dense product left is
+//     O^T = S0 X~^T + ACC^T      (dv x T, K = dk)
+// per (sequence, value head), which runs on the MFMA units with a bf16 hi/lo
+// split of both operands (three bf16 products per tile, fp32 accumulation,
+// ~1e-5 relative error).
 //
-// Workgroup = (dv slice, value head h, sequence b); 256 threads.
-//   phase 0  metadata of the tree in canonical order -> LDS
-//   phase 1  conv + SiLU + L2-norm of q, k along each node's path; k~ -> LDS,
-//            q~ stays in the registers of the node's lane quad
-//   phase 2  pull-back (4 lanes per node, quad reductions), coefficients -> LDS
-//   phase 3  MFMA product; v~ is computed from the raw values on the fly in
-//            the B-operand registers.
+// Workgroup = (dv slice, key head g with HPW of its value heads, sequence b),
+// 512 threads.  Wave w owns the 16 tree positions [16w, 16w+16) of the
+// canonical (depth, index) order; lane (l16, lg) of a wave holds, for node
+// 16w + l16, the key channels 32kb + 8lg + e and the value channels
+// 16n + 4lg + e.  That is exactly the MFMA B-operand layout of X~^T and the
+// accumulator layout of O^T for v_mfma_f32_16x16x32_bf16, so the pulled-back
+// queries and the value accumulators never leave registers.
+//   phase 0  tree metadata in canonical order -> LDS; prefetch S0 and raw v
+//            of the first head into registers
+//   phase 1  conv + SiLU + L2-norm of q and k along each node's path (raw
+//            rows staged in LDS); q~ stays in registers, k~ -> LDS (fp32)
+//   per value head:
+//     2a/b   raw v -> LDS, conv + SiLU -> v~ in LDS (fp32); prefetch the next
+//            head's raw v
+//     2c     pull-back with k~, v~ gathered from LDS (4 lanes per node)
+//     2d     S0 (prefetched) -> LDS as bf16 hi/lo planes; prefetch next S0
+//     2e     MFMA O^T = S0 X~^T + ACC^T, store
 #include "gdn_internal.h"
 
 namespace gdn {
@@ -35,14 +44,13 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kVT = 256;                // threads per workgroup
-constexpr int kVMaxT = 128;             // tree slots supported
-constexpr int kQuads = kVT / 4;         // lane quads = nodes in flight
-constexpr int kNPR = kVMaxT / kQuads;   // nodes per quad
-constexpr int kKPad = 4;                // row padding (floats) of the k~/x~ tile
+constexpr int kVT = 512;        // threads per workgroup (8 waves)
+constexpr int kVMaxT = 128;     // tree slots supported = 8 waves x 16 nodes
+constexpr int kKPad = 4;        // fp32 row padding of the k~ and v~ tiles
+constexpr int kSPad = 8;        // bf16 row padding of the S0 planes
 
 struct VerifyParams {
-  int B, T, Hk, Hv, nslices;
+  int B, T, Hk, Hv, nslices, hpw;
   float scale;
   const void* meta;
   const void *q, *k, *v, *alpha, *beta;
@@ -66,6 +74,20 @@ __device__ __forceinline__ void split8(const float (&x)[8], bf16x8& hi, bf16x8& 
   lo = __builtin_bit_cast(bf16x8, l);
 }
 
+// 4 floats -> packed bf16 hi (2 dwords) and lo (2 dwords), truncation split
+__device__ __forceinline__ void split4(float4 x, uint2& hi, uint2& lo) {
+  const float xs[4] = {x.x, x.y, x.z, x.w};
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t u = __float_as_uint(xs[e]);
+    h[e] = u & 0xffff0000u;
+    l[e] = __float_as_uint(xs[e] - __uint_as_float(h[e])) & 0xffff0000u;
+  }
+  hi = make_uint2((h[0] >> 16) | h[1], (h[2] >> 16) | h[3]);
+  lo = make_uint2((l[0] >> 16) | l[1], (l[2] >> 16) | l[3]);
+}
+
 __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const bf16x8& bh,
                                        const bf16x8& bl, f32x4 c) {
   c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, c, 0, 0, 0);
@@ -74,382 +96,427 @@ __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const
   return c;
 }
 
-__host__ __device__ inline int verify_ncoef(int T) { return ((T * (T + 1) / 2) + 3) & ~3; }
+// 8 consecutive input elements as floats (16 B for bf16, 32 B for fp32)
+__device__ __forceinline__ void ld8(const float* p, float (&x)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+__device__ __forceinline__ void ld8(const BF16* p, float (&x)[8]) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[2 * e] = __uint_as_float(w[e] << 16);
+    x[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+  }
+}
 
-// LDS bytes for a tree of T slots and key dim DK.
-__host__ __device__ inline size_t verify_smem_bytes(int T, int DK) {
-  int TP2 = (T + 31) & ~31;
-  size_t b = size_t(TP2) * (DK + kKPad) * 4;  // k~ / x~ tile
-  b += size_t(4 * kVMaxT + 4) * 4;            // order, parent pos, depth, offsets
-  b += size_t(2 * kVMaxT + 8 * DK) * 4;       // alpha, beta, q/k conv weights
-  b += size_t(verify_ncoef(T)) * 8;           // coefficients + their positions
-  return b;
+// LDS regions (bytes) for a tree of T slots, key dim DK and value slice DVS
+struct VerifySmem {
+  size_t rk, rv, meta, total;
+};
+__host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
+  const int TP = (T + 15) & ~15;
+  VerifySmem s;
+  const size_t k_tile = size_t(TP) * (DK + kKPad) * 4;    // k~ (fp32)
+  const size_t k_stage = size_t(T + 3) * DK * 4;           // raw q or k rows + 3 conv-state rows
+  s.rk = k_tile > k_stage ? k_tile : k_stage;
+  const size_t v_tile = size_t(TP) * (DVS + kKPad) * 4;   // v~ (fp32)
+  const size_t v_stage = size_t(T + 3) * DVS * 4;          // raw v rows + 3 conv-state rows
+  const size_t s_tile = size_t(DVS) * (DK + kSPad) * 2 * 2;  // S0 bf16 hi + lo planes
+  s.rv = v_tile > v_stage ? v_tile : v_stage;
+  s.rv = s.rv > s_tile ? s.rv : s_tile;
+  s.meta = size_t(3 * kVMaxT) * 4                          // order, parent pos, depth
+           + size_t(2 * kVMaxT) * 4                        // alpha, beta of the current head
+           + size_t(8 * DK) * 4 + size_t(4 * DVS) * 4;     // q/k and v conv weights
+  s.total = s.rk + s.rv + s.meta;
+  return s;
+}
+
+// Issue the loads of this thread's share of S0[b][h][c0 .. c0+DVS][0 .. DK).
+template <int DK, int NS0>
+__device__ __forceinline__ void prefetch_s0(const float* S0bh, int DVS, int tid, float4 (&pf)[NS0]) {
+  const int n4 = DVS * DK / 4;
+#pragma unroll
+  for (int j = 0; j < NS0; ++j) {
+    const int idx = j * kVT + tid;
+    pf[j] = idx < n4 ? reinterpret_cast<const float4*>(S0bh)[idx] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+// Issue the loads of this thread's share of the raw values v[b][.][h][c0 .. c0+DVS)
+// for the T nodes (16-byte chunks, node-major).
+template <typename TIn, int NVC>
+__device__ __forceinline__ void prefetch_v(const TIn* vin, size_t node_stride, const int* s_ord,
+                                           int T, int DVS, int tid, uint4 (&pf)[NVC]) {
+  constexpr int EPC = 16 / sizeof(TIn);  // elements per 16-byte chunk
+  const int sh = __builtin_ctz(DVS / EPC);  // log2 of the chunks per node row (a power of two)
+#pragma unroll
+  for (int j = 0; j < NVC; ++j) {
+    const int idx = j * kVT + tid;
+    const int p = idx >> sh, c = idx & ((1 << sh) - 1);
+    pf[j] = p < T ? *reinterpret_cast<const uint4*>(vin + size_t(s_ord[p]) * node_stride + c * EPC)
+                  : make_uint4(0, 0, 0, 0);
+  }
+}
+
+// Write one 16-byte chunk of raw inputs (8 bf16 or 4 fp32) to LDS as fp32.
+__device__ __forceinline__ void store_chunk_f32(float* dst, uint4 u, const BF16*) {
+  *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                                                __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+  *reinterpret_cast<float4*>(dst + 4) = make_float4(__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xffff0000u),
+                                                    __uint_as_float(u.w << 16), __uint_as_float(u.w & 0xffff0000u));
+}
+__device__ __forceinline__ void store_chunk_f32(float* dst, uint4 u, const float*) {
+  *reinterpret_cast<float4*>(dst) =
+      make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
 }
 
 template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int KROW = DK + kKPad;
-  constexpr int CPL = DK / 4;   // channels per lane
-  constexpr int NCH = DK / 16;  // 4-channel chunks per lane
-  constexpr int KS1 = (DK + 31) / 32;
-  constexpr int NPW_MAX = DV / 64 > 1 ? DV / 64 : 1;
-  constexpr int MPW_MAX = kVMaxT / 16;
+  constexpr int KB = DK >= 32 ? DK / 32 : 1;  // 32-wide key blocks (dk = 16 is zero-padded)
+  constexpr int KPL = 8 * KB;                 // key channels per lane (padding included)
+  constexpr int KROW = DK + kKPad;            // k~ row stride (floats)
+  constexpr int NT_MAX = DV / 16;             // 16-row value tiles
+  constexpr int EPC = 16 / sizeof(TIn);
+  constexpr int NS0 = (DV * DK / 4 + kVT - 1) / kVT;                   // S0 float4 per thread
+  constexpr int NVC = (kVMaxT * DV / EPC + kVT - 1) / kVT;             // raw-v chunks per thread
 
   const int T = p.T;
-  const int slice = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int TP = (T + 15) & ~15;
   const int Hk = p.Hk, Hv = p.Hv;
-  const int g = h * Hk / Hv;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int G = Hv / Hk;
+  const int nhg = G / p.hpw;
+  const int b = blockIdx.z;
+  const int g = blockIdx.y / nhg;
+  const int h0 = g * G + (blockIdx.y % nhg) * p.hpw;
   const int DVS = DV / p.nslices;
-  const int TP2 = (T + 31) & ~31;
+  const int c0 = blockIdx.x * DVS;   // first value channel of this slice
+  const int NT = DVS / 16;
   const int C = 2 * Hk * DK + Hv * DV;
   const size_t orow = size_t(Hv) * DV;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, lg = lane >> 4;
+  const int pos = wave * 16 + l16;   // tree position owned by this lane
 
-  float* s_x = reinterpret_cast<float*>(smem);
-  int* s_ord = reinterpret_cast<int*>(s_x + TP2 * KROW);
+  const VerifySmem L = verify_smem(T, DK, DVS);
+  float* s_k = reinterpret_cast<float*>(smem);                 // [TP][KROW]
+  unsigned char* s_rv = smem + L.rk;                           // raw v / v~ / S0 planes
+  float* s_v = reinterpret_cast<float*>(s_rv);                 // [TP][DVS + kKPad]
+  int* s_ord = reinterpret_cast<int*>(smem + L.rk + L.rv);
   int* s_ppos = s_ord + kVMaxT;
   int* s_dep = s_ppos + kVMaxT;
-  int* s_off = s_dep + kVMaxT;
-  float* s_al = reinterpret_cast<float*>(s_off + kVMaxT + 4);
+  float* s_al = reinterpret_cast<float*>(s_dep + kVMaxT);
   float* s_be = s_al + kVMaxT;
-  float* s_w = s_be + kVMaxT;  // [2][DK][4]
-  float* s_coef = s_w + 8 * DK;
-  int* s_cpos = reinterpret_cast<int*>(s_coef + verify_ncoef(T));
+  float* s_wqk = s_be + kVMaxT;                                // [2][DK][4]
+  float* s_wv = s_wqk + 8 * DK;                                // [DVS][4]
+  const int VROW = DVS + kKPad;
 
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
   const int status = m.status[b];
   const int nv = m.nvalid[b];
   if (status != GDN_TREE_OK) {
-    for (int idx = tid; idx < T * DVS; idx += kVT) {
-      int i = idx / DVS, c = idx % DVS;
-      p.out[(size_t(b) * T + i) * orow + size_t(h) * DV + slice * DVS + c] = 0.0f;
-    }
+    for (int hh = 0; hh < p.hpw; ++hh)
+      for (int idx = tid; idx < T * DVS; idx += kVT) {
+        const int i = idx / DVS, c = idx % DVS;
+        p.out[(size_t(b) * T + i) * orow + size_t(h0 + hh) * DV + c0 + c] = 0.0f;
+      }
     return;
   }
 
-  // ---------------- phase 0: tree metadata in canonical order --------------
+  // ---------------- phase 0 ----------------
+  if (tid < T) {
+    int node = m.order[b * T + tid];
+    node = (node >= 0 && node < T) ? node : 0;  // prepare writes a permutation
+    const bool real = tid < nv;
+    s_ord[tid] = node;
+    s_dep[tid] = real ? m.depth[b * T + node] : -1;
+    const int par = m.parent[b * T + node];
+    s_ppos[tid] = (real && par >= 0 && par < T) ? m.pos[b * T + par] : -1;
+  }
+  for (int i = tid; i < 8 * DK; i += kVT) {  // tap-major: s_wqk[part][w][c]
+    const int part = i / (4 * DK), w = (i / DK) & 3, c = i % DK;
+    s_wqk[i] = p.conv_w[size_t(part * Hk * DK + g * DK + c) * 4 + w];
+  }
+  float4 s0pf[NS0];
+  prefetch_s0<DK>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, DVS, tid, s0pf);
+  __syncthreads();
+  const TIn* vin = static_cast<const TIn*>(p.v);
+  uint4 vpf[NVC];
+  prefetch_v<TIn>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, DVS, tid, vpf);
+
+  // ---------------- phase 1: q~ and k~ ----------------
+  // Raw rows are staged in LDS as fp32, in canonical order, followed by the
+  // three conv-state slots, so that every conv tap is an LDS row: tap w of a
+  // node at depth d is row tap[w] if d - 3 + w >= 0, else conv-state row
+  // T + d + w (slot d + w; slot 2 is the most recent token).
+  const bool active = pos < nv;
+  int trow[4] = {0, 0, 0, 0};
+  int dep = -1;
+  if (active) {
+    dep = s_dep[pos];
+    int t2 = s_ppos[pos];
+    int t1 = t2 >= 0 ? s_ppos[t2] : -1;
+    int t0 = t1 >= 0 ? s_ppos[t1] : -1;
+    const int tp[4] = {t0, t1, t2, pos};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) trow[w] = (dep - 3 + w >= 0) ? tp[w] : T + dep + w;
+  }
+  float qh[KPL];  // q~ of this lane's node, later the start of the pull-back
+  float kh[KPL];
+  const TIn* qk_src[2] = {static_cast<const TIn*>(p.q), static_cast<const TIn*>(p.k)};
+  const size_t qk_row = size_t(Hk) * DK;
+  float* s_stage = s_k;  // [T + 3][DK] fp32
+#pragma unroll 1
+  for (int part = 0; part < 2; ++part) {
+    const TIn* src = qk_src[part] + size_t(b) * T * qk_row + size_t(g) * DK;
+    const float* cs = p.conv_state + size_t(b) * 3 * C + part * Hk * DK + g * DK;
+    constexpr int cpr = DK / 4;  // float4 chunks per row
+    for (int idx = tid; idx < (T + 3) * cpr; idx += kVT) {
+      const int row = idx / cpr, c = (idx % cpr) * 4;
+      const float4 x = row < T ? ld4(src + size_t(s_ord[row]) * qk_row + c)
+                               : ld4(cs + size_t(row - T) * C + c);
+      *reinterpret_cast<float4*>(s_stage + row * DK + c) = x;
+    }
+    __syncthreads();
+    float y[KPL];
+#pragma unroll
+    for (int c = 0; c < KPL; ++c) y[c] = 0.0f;
+    if (active) {
+      const float* wpart = s_wqk + part * 4 * DK;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const int c = 32 * kb + 8 * lg;
+        if (c < DK) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            float x[8], wt[8];
+            ld8(s_stage + trow[w] * DK + c, x);
+            ld8(wpart + w * DK + c, wt);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) y[8 * kb + e] += wt[e] * x[e];
+          }
+        }
+      }
+    }
+    float ss = 0.0f;
+#pragma unroll
+    for (int c = 0; c < KPL; ++c) {
+      y[c] = silu(y[c]);  // silu(0) = 0 keeps padding channels at zero
+      ss += y[c] * y[c];
+    }
+    ss += __shfl_xor(ss, 16);
+    ss += __shfl_xor(ss, 32);
+    const float inv = rsqrt_hw(ss + 1e-6f);
+    if (part == 0) {
+#pragma unroll
+      for (int c = 0; c < KPL; ++c) qh[c] = active ? y[c] * inv : 0.0f;
+    } else {
+#pragma unroll
+      for (int c = 0; c < KPL; ++c) kh[c] = active ? y[c] * inv : 0.0f;
+    }
+    __syncthreads();  // staged rows consumed
+  }
+  if (active) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const int c = 32 * kb + 8 * lg;
+      if (c < DK) {
+        *reinterpret_cast<float4*>(s_k + pos * KROW + c) =
+            make_float4(kh[8 * kb], kh[8 * kb + 1], kh[8 * kb + 2], kh[8 * kb + 3]);
+        *reinterpret_cast<float4*>(s_k + pos * KROW + c + 4) =
+            make_float4(kh[8 * kb + 4], kh[8 * kb + 5], kh[8 * kb + 6], kh[8 * kb + 7]);
+      }
+    }
+  }
+
+  // ---------------- phase 2: one value head at a time ----------------
   const TIn* alpha = static_cast<const TIn*>(p.alpha);
   const TIn* beta = static_cast<const TIn*>(p.beta);
-  if (tid < T) {
-    const int i = tid;
-    int node = m.order[b * T + i];
-    node = (node >= 0 && node < T) ? node : 0;  // metadata written by prepare is a permutation
-    const bool real = i < nv;
-    s_ord[i] = node;
-    s_dep[i] = real ? m.depth[b * T + node] : -1;
-    const int par = m.parent[b * T + node];
-    s_ppos[i] = (real && par >= 0 && par < T) ? m.pos[b * T + par] : -1;
-    const size_t ab = (size_t(b) * T + node) * Hv + h;
-    s_al[i] = ld(alpha, ab);
-    s_be[i] = ld(beta, ab);
-  }
-  for (int i = tid; i < 8 * DK; i += kVT) {
-    const int part = i / (4 * DK), rem = i % (4 * DK);
-    const int ch = part * Hk * DK + g * DK + rem / 4;
-    s_w[i] = p.conv_w[size_t(ch) * 4 + (rem & 3)];
-  }
-  __syncthreads();
-  if (wave == 0) {  // exclusive scan of (depth + 1) over real positions
-    const int i0 = 2 * lane, i1 = 2 * lane + 1;
-    const int v0 = i0 < nv ? s_dep[i0] + 1 : 0;
-    const int v1 = i1 < nv ? s_dep[i1] + 1 : 0;
-    int sum = v0 + v1;
+  for (int hh = 0; hh < p.hpw; ++hh) {
+    const int h = h0 + hh;
+    // 2a: raw v rows (prefetched) + 3 conv-state rows -> LDS as fp32
+    //     [T + 3][DVS]; gates and v conv weights -> LDS
+    const int vch0 = 2 * Hk * DK + h * DV + c0;  // conv channel of v[h][c0]
+    {
+      float* s_vs = reinterpret_cast<float*>(s_rv);
+      const int sh = __builtin_ctz(DVS / EPC);
 #pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      int t = __shfl_up(sum, o);
-      if (lane >= o) sum += t;
-    }
-    const int excl = sum - v0 - v1;
-    s_off[i0] = excl;
-    s_off[i1] = excl + v0;
-  }
-  __syncthreads();
-
-  // ---------------- phase 1: conv / SiLU / L2-norm of q and k --------------
-  const int quad = tid >> 2, q4 = tid & 3;
-  const TIn* qin = static_cast<const TIn*>(p.q);
-  const TIn* kin = static_cast<const TIn*>(p.k);
-  const size_t qk_row = size_t(Hk) * DK;
-  float qh[kNPR][CPL];
-#pragma unroll
-  for (int r = 0; r < kNPR; ++r) {
-    const int pp = quad + r * kQuads;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) qh[r][c] = 0.0f;
-    if (pp < nv) {
-      const int d = s_dep[pp];
-      int tap[4];
-      tap[3] = pp;
-      tap[2] = s_ppos[pp];
-      tap[1] = tap[2] >= 0 ? s_ppos[tap[2]] : -1;
-      tap[0] = tap[1] >= 0 ? s_ppos[tap[1]] : -1;
-      float yq[CPL], yk[CPL];
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) yq[c] = yk[c] = 0.0f;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const int mm = d - 3 + w;
-        const TIn* qrow = nullptr;
-        const TIn* krow = nullptr;
-        const float* cs = nullptr;
-        if (mm >= 0) {
-          const size_t node = s_ord[tap[w]];
-          qrow = qin + (size_t(b) * T + node) * qk_row + size_t(g) * DK;
-          krow = kin + (size_t(b) * T + node) * qk_row + size_t(g) * DK;
-        } else {
-          cs = p.conv_state + (size_t(b) * 3 + (3 + mm)) * C;
-        }
-#pragma unroll
-        for (int u = 0; u < NCH; ++u) {
-          const int c = 16 * u + 4 * q4;
-          float4 xq, xk;
-          if (mm >= 0) {
-            xq = ld4(qrow + c);
-            xk = ld4(krow + c);
-          } else {
-            xq = ld4(cs + g * DK + c);
-            xk = ld4(cs + Hk * DK + g * DK + c);
-          }
-          const float xqa[4] = {xq.x, xq.y, xq.z, xq.w};
-          const float xka[4] = {xk.x, xk.y, xk.z, xk.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            yq[4 * u + e] += s_w[(c + e) * 4 + w] * xqa[e];
-            yk[4 * u + e] += s_w[4 * DK + (c + e) * 4 + w] * xka[e];
-          }
+      for (int j = 0; j < NVC; ++j) {
+        const int idx = j * kVT + tid;
+        if (idx < (T << sh)) {
+          const int row = idx >> sh, c = (idx & ((1 << sh) - 1)) * EPC;
+          store_chunk_f32(s_vs + row * DVS + c, vpf[j], static_cast<const TIn*>(nullptr));
         }
       }
-      float sq = 0.0f, sk = 0.0f;
+      const float* cs = p.conv_state + size_t(b) * 3 * C + vch0;
+      for (int i = tid; i < 3 * DVS; i += kVT) s_vs[(T + i / DVS) * DVS + i % DVS] = cs[size_t(i / DVS) * C + i % DVS];
+    }
+    if (tid < T) {
+      const size_t ab = (size_t(b) * T + s_ord[tid]) * Hv + h;
+      s_al[tid] = ld(alpha, ab);
+      s_be[tid] = ld(beta, ab);
+    }
+    for (int i = tid; i < 4 * DVS; i += kVT)  // tap-major: s_wv[w][c]
+      s_wv[i] = p.conv_w[size_t(vch0 + i % DVS) * 4 + i / DVS];
+    __syncthreads();
+    // 2b: v~ for this lane's node and value channels 16n + 4lg + e
+    float vt[4 * NT_MAX];
+    {
+      const float* s_vs = reinterpret_cast<const float*>(s_rv);
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        yq[c] = silu(yq[c]);
-        yk[c] = silu(yk[c]);
-        sq += yq[c] * yq[c];
-        sk += yk[c] * yk[c];
-      }
-      sq += __shfl_xor(sq, 1);
-      sq += __shfl_xor(sq, 2);
-      sk += __shfl_xor(sk, 1);
-      sk += __shfl_xor(sk, 2);
-      const float iq = 1.0f / sqrtf(sq + 1e-6f);
-      const float ik = 1.0f / sqrtf(sk + 1e-6f);
+      for (int n = 0; n < NT_MAX; ++n) {
 #pragma unroll
-      for (int u = 0; u < NCH; ++u) {
-        const int c = 16 * u + 4 * q4;
+        for (int e = 0; e < 4; ++e) vt[4 * n + e] = 0.0f;
+        if (active && n < NT) {
+          const int c = 16 * n + 4 * lg;
+          float y[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) qh[r][4 * u + e] = yq[4 * u + e] * iq;
-        *reinterpret_cast<float4*>(s_x + pp * KROW + c) =
-            make_float4(yk[4 * u] * ik, yk[4 * u + 1] * ik, yk[4 * u + 2] * ik, yk[4 * u + 3] * ik);
+          for (int w = 0; w < 4; ++w) {
+            const float4 x = ld4(s_vs + trow[w] * DVS + c);
+            const float4 wt = ld4(s_wv + w * DVS + c);
+            y[0] += wt.x * x.x;
+            y[1] += wt.y * x.y;
+            y[2] += wt.z * x.z;
+            y[3] += wt.w * x.w;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) vt[4 * n + e] = silu(y[e]);
+        }
       }
     }
-  }
-  __syncthreads();
-
-  // ---------------- phase 2: query pull-back along each path ----------------
+    __syncthreads();  // raw v consumed
+    if (active) {
 #pragma unroll
-  for (int r = 0; r < kNPR; ++r) {
-    const int pp = quad + r * kQuads;
-    if (pp < nv) {
-      float rr = 1.0f;
-      int t = pp;
-      const int off = s_off[pp];
+      for (int n = 0; n < NT_MAX; ++n)
+        if (n < NT)
+          *reinterpret_cast<float4*>(s_v + pos * VROW + 16 * n + 4 * lg) =
+              make_float4(vt[4 * n], vt[4 * n + 1], vt[4 * n + 2], vt[4 * n + 3]);
+    }
+    if (hh + 1 < p.hpw)
+      prefetch_v<TIn>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, DVS, tid, vpf);
+    __syncthreads();
+
+    // 2c: query pull-back along the path, leaf to root
+    float x[KPL];
+    float acc[4 * NT_MAX];
+#pragma unroll
+    for (int c = 0; c < KPL; ++c) x[c] = qh[c];
+#pragma unroll
+    for (int c = 0; c < 4 * NT_MAX; ++c) acc[c] = 0.0f;
+    float r = 1.0f;
+    {
+      int t = active ? pos : -1;
       // a path has at most T nodes; the bound also ends the walk on corrupt metadata
-      for (int step = 0; t >= 0 && step < T; ++step) {
-        const float* krow = s_x + t * KROW;
-        float kv[CPL];
-        float s = 0.0f;
+      for (int step = 0; step < T; ++step) {
+        if (t < 0) break;
+        float kt[KPL];
 #pragma unroll
-        for (int u = 0; u < NCH; ++u) {
-          const float4 k4 = *reinterpret_cast<const float4*>(krow + 16 * u + 4 * q4);
-          kv[4 * u] = k4.x;
-          kv[4 * u + 1] = k4.y;
-          kv[4 * u + 2] = k4.z;
-          kv[4 * u + 3] = k4.w;
+        for (int kb = 0; kb < KB; ++kb) {
+          const int c = 32 * kb + 8 * lg;
+          float k8[8];
+          if (c < DK) {
+            ld8(s_k + t * KROW + c, k8);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) k8[e] = 0.0f;
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) kt[8 * kb + e] = k8[e];
         }
+        float s0 = 0.f, s1 = 0.f;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) s += kv[c] * qh[r][c];
-        s += __shfl_xor(s, 1);
-        s += __shfl_xor(s, 2);
+        for (int c = 0; c < KPL; c += 2) {
+          s0 += kt[c] * x[c];
+          s1 += kt[c + 1] * x[c + 1];
+        }
+        float s = s0 + s1;
+        s += __shfl_xor(s, 16);
+        s += __shfl_xor(s, 32);
         const float bs = s_be[t] * s;
-        if (q4 == 0) {
-          const int slot = off + s_dep[t];
-          s_coef[slot] = rr * bs;
-          s_cpos[slot] = t;
-        }
+        const float rbs = r * bs;
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) qh[r][c] -= bs * kv[c];
-        rr *= s_al[t];
+        for (int c = 0; c < KPL; ++c) x[c] -= bs * kt[c];
+#pragma unroll
+        for (int n = 0; n < NT_MAX; ++n) {
+          if (n < NT) {
+            const float4 v4 = *reinterpret_cast<const float4*>(s_v + t * VROW + 16 * n + 4 * lg);
+            acc[4 * n] += rbs * v4.x;
+            acc[4 * n + 1] += rbs * v4.y;
+            acc[4 * n + 2] += rbs * v4.z;
+            acc[4 * n + 3] += rbs * v4.w;
+          }
+        }
+        r *= s_al[t];
         t = s_ppos[t];
       }
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) qh[r][c] *= rr;  // a_i * x~_i
     }
-  }
-  __syncthreads();  // every pull-back has finished reading k~
 #pragma unroll
-  for (int r = 0; r < kNPR; ++r) {
-    const int pp = quad + r * kQuads;
-    if (pp < TP2) {
-#pragma unroll
-      for (int u = 0; u < NCH; ++u) {
-        const int c = 16 * u + 4 * q4;
-        *reinterpret_cast<float4*>(s_x + pp * KROW + c) =
-            make_float4(qh[r][4 * u], qh[r][4 * u + 1], qh[r][4 * u + 2], qh[r][4 * u + 3]);
-      }
-    }
-  }
-  __syncthreads();
+    for (int c = 0; c < KPL; ++c) x[c] *= r;  // a_i x~_i
+    __syncthreads();  // v~ consumed
 
-  // ---------------- phase 3: O = scale [a X~ | C] [S0^T ; V~] on MFMA -------
-  const int NTS = DVS / 16;
-  const int WN = NTS >= 4 ? 4 : NTS;
-  const int WM = 4 / WN;
-  const int wn = wave % WN, wm = wave / WN;
-  const int NPW = NTS / WN;
-  const int MT = TP2 / 16;
-  const int l16 = lane & 15, lg = lane >> 4;
-
-  f32x4 acc[NPW_MAX][MPW_MAX];
+    // 2d: S0 of this head -> LDS as bf16 hi/lo planes [DVS][DK + kSPad]
+    {
+      uint16_t* s_hi = reinterpret_cast<uint16_t*>(s_rv);
+      uint16_t* s_lo = s_hi + DVS * (DK + kSPad);
 #pragma unroll
-  for (int ni = 0; ni < NPW_MAX; ++ni)
-#pragma unroll
-    for (int mi = 0; mi < MPW_MAX; ++mi) acc[ni][mi] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // part 1: a X~ S0^T   (K = dk)
-  const float* S0bh = p.S0 + (size_t(b) * Hv + h) * size_t(DV) * DK;
-#pragma unroll
-  for (int ks = 0; ks < KS1; ++ks) {
-    const int k0 = ks * 32 + 8 * lg;
-    bf16x8 bh[NPW_MAX], bl[NPW_MAX];
-#pragma unroll
-    for (int ni = 0; ni < NPW_MAX; ++ni) {
-      if (ni < NPW) {
-        const int rcol = slice * DVS + (wn + ni * WN) * 16 + l16;
-        float xs[8];
-        if (k0 < DK) {
-          const float4 a0 = ld4(S0bh + size_t(rcol) * DK + k0);
-          const float4 a1 = ld4(S0bh + size_t(rcol) * DK + k0 + 4);
-          xs[0] = a0.x; xs[1] = a0.y; xs[2] = a0.z; xs[3] = a0.w;
-          xs[4] = a1.x; xs[5] = a1.y; xs[6] = a1.z; xs[7] = a1.w;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) xs[e] = 0.0f;
+      for (int j = 0; j < NS0; ++j) {
+        const int idx = j * kVT + tid;
+        if (idx < DVS * DK / 4) {
+          const int row = idx / (DK / 4), col = (idx % (DK / 4)) * 4;
+          uint2 hi, lo;
+          split4(s0pf[j], hi, lo);
+          *reinterpret_cast<uint2*>(s_hi + row * (DK + kSPad) + col) = hi;
+          *reinterpret_cast<uint2*>(s_lo + row * (DK + kSPad) + col) = lo;
         }
-        split8(xs, bh[ni], bl[ni]);
       }
     }
-#pragma unroll
-    for (int mi = 0; mi < MPW_MAX; ++mi) {
-      const int mt = wm + mi * WM;
-      if (mt < MT) {
-        const int row = mt * 16 + l16;
-        float xa[8];
-        if (k0 < DK) {
-          const float4 a0 = *reinterpret_cast<const float4*>(s_x + row * KROW + k0);
-          const float4 a1 = *reinterpret_cast<const float4*>(s_x + row * KROW + k0 + 4);
-          xa[0] = a0.x; xa[1] = a0.y; xa[2] = a0.z; xa[3] = a0.w;
-          xa[4] = a1.x; xa[5] = a1.y; xa[6] = a1.z; xa[7] = a1.w;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) xa[e] = 0.0f;
-        }
-        bf16x8 ah, al;
-        split8(xa, ah, al);
-#pragma unroll
-        for (int ni = 0; ni < NPW_MAX; ++ni)
-          if (ni < NPW) acc[ni][mi] = mfma3(ah, al, bh[ni], bl[ni], acc[ni][mi]);
-      }
-    }
-  }
+    if (hh + 1 < p.hpw)
+      prefetch_s0<DK>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, DVS, tid, s0pf);
+    __syncthreads();
 
-  // part 2: C V~   (K = tree positions; C lower triangular)
-  const TIn* vin = static_cast<const TIn*>(p.v);
-  const int vbase = 2 * Hk * DK + h * DV;  // conv channel of v[h][0]
-  for (int ks = 0; ks < TP2 / 32; ++ks) {
-    const int j0 = ks * 32 + 8 * lg;
-    bf16x8 bh[NPW_MAX], bl[NPW_MAX];
+    // 2e: O^T = S0 X~^T + ACC^T on MFMA; store
+    if (wave * 16 < TP) {
+      bf16x8 xh[KB], xl[KB];
 #pragma unroll
-    for (int ni = 0; ni < NPW_MAX; ++ni) {
-      if (ni < NPW) {
-        const int rcol = slice * DVS + (wn + ni * WN) * 16 + l16;
-        const float4 wv = ld4(p.conv_w + size_t(vbase + rcol) * 4);
-        const float wva[4] = {wv.x, wv.y, wv.z, wv.w};
-        float xs[8];
+      for (int kb = 0; kb < KB; ++kb) {
+        float x8[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int j = j0 + e;
-          float y = 0.0f;
-          if (j < nv) {
-            const int d = s_dep[j];
-            int t = j;
+        for (int e = 0; e < 8; ++e) x8[e] = x[8 * kb + e];
+        split8(x8, xh[kb], xl[kb]);
+      }
+      const uint16_t* s_hi = reinterpret_cast<const uint16_t*>(s_rv);
+      const uint16_t* s_lo = s_hi + DVS * (DK + kSPad);
+      const int node = pos < T ? s_ord[pos] : 0;
+      float* orow_p = p.out + (size_t(b) * T + node) * orow + size_t(h) * DV + c0;
 #pragma unroll
-            for (int w = 3; w >= 0; --w) {
-              const int mm = d - 3 + w;
-              float x;
-              if (mm >= 0) {
-                x = ld(vin, (size_t(b) * T + s_ord[t]) * orow + size_t(h) * DV + rcol);
-                if (w > 0) t = s_ppos[t];
-              } else {
-                x = p.conv_state[(size_t(b) * 3 + (3 + mm)) * C + vbase + rcol];
-              }
-              y += wva[w] * x;
+      for (int n = 0; n < NT_MAX; ++n) {
+        if (n < NT) {
+          f32x4 d = {acc[4 * n], acc[4 * n + 1], acc[4 * n + 2], acc[4 * n + 3]};
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) {
+            const int c = 32 * kb + 8 * lg;
+            bf16x8 ah, al;
+            if (c < DK) {
+              const int off = (16 * n + l16) * (DK + kSPad) + c;
+              ah = *reinterpret_cast<const bf16x8*>(s_hi + off);
+              al = *reinterpret_cast<const bf16x8*>(s_lo + off);
+            } else {
+              ah = bf16x8{};
+              al = bf16x8{};
             }
-            y = silu(y);
+            d = mfma3(ah, al, xh[kb], xl[kb], d);
           }
-          xs[e] = y;
-        }
-        split8(xs, bh[ni], bl[ni]);
-      }
-    }
-#pragma unroll
-    for (int mi = 0; mi < MPW_MAX; ++mi) {
-      const int mt = wm + mi * WM;
-      if (mt < MT && ks * 32 <= mt * 16 + 15) {
-        const int i = mt * 16 + l16;
-        const int di = i < nv ? s_dep[i] : -1;
-        const int offi = s_off[i];
-        float xa[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int j = j0 + e;
-          float cv = 0.0f;
-          if (di >= 0 && j <= i) {
-            const int dj = s_dep[j];
-            if (dj <= di) {
-              const int slot = offi + dj;
-              if (s_cpos[slot] == j) cv = s_coef[slot];
-            }
-          }
-          xa[e] = cv;
-        }
-        bf16x8 ah, al;
-        split8(xa, ah, al);
-#pragma unroll
-        for (int ni = 0; ni < NPW_MAX; ++ni)
-          if (ni < NPW) acc[ni][mi] = mfma3(ah, al, bh[ni], bl[ni], acc[ni][mi]);
-      }
-    }
-  }
-
-  // store: tile row 4*lg+e, column l16
-#pragma unroll
-  for (int ni = 0; ni < NPW_MAX; ++ni) {
-    if (ni >= NPW) continue;
-    const int rcol = slice * DVS + (wn + ni * WN) * 16 + l16;
-#pragma unroll
-    for (int mi = 0; mi < MPW_MAX; ++mi) {
-      const int mt = wm + mi * WM;
-      if (mt >= MT) continue;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int i = mt * 16 + 4 * lg + e;
-        if (i < T) {
-          const size_t node = s_ord[i];
-          p.out[(size_t(b) * T + node) * orow + size_t(h) * DV + rcol] = acc[ni][mi][e] * p.scale;
+          if (pos < T)
+            *reinterpret_cast<float4*>(orow_p + 16 * n + 4 * lg) =
+                make_float4(d[0] * p.scale, d[1] * p.scale, d[2] * p.scale, d[3] * p.scale);
         }
       }
     }
+    __syncthreads();  // S0 planes consumed before the next head reuses the region
   }
 }
 
@@ -471,21 +538,29 @@ static int launch_verify_t(const VerifyArgs& a, hipStream_t stream) {
   p.conv_state = a.conv_state;
   p.S0 = a.S0;
   p.out = a.out;
-  // split the value dim across workgroups while the grid is small
-  int ns = 1;
-  while (size_t(a.B) * a.Hv * ns < 256 && DV / (2 * ns) >= 32) ns *= 2;
+  // Work split: all value heads of a key head share one workgroup (one q/k
+  // conv) when that still gives >= 256 workgroups; otherwise one value head
+  // per workgroup and, for small batches, the value dim split across slices.
+  const int G = a.Hv / a.Hk;
+  int hpw = G, ns = 1;
+  if (size_t(a.B) * a.Hk < 256) {
+    hpw = 1;
+    while (size_t(a.B) * a.Hv * ns < 256 && DV / (2 * ns) >= 32) ns *= 2;
+  }
+  p.hpw = hpw;
   p.nslices = ns;
-  const size_t smem = verify_smem_bytes(a.T, DK);
+  const size_t smem = verify_smem(a.T, DK, DV / ns).total;
   static bool attr_done = false;
   if (!attr_done) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&verify_kernel<DK, DV, TIn>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(verify_smem_bytes(kVMaxT, DK)));
+                                       int(verify_smem(kVMaxT, DK, DV).total));
     if (e != hipSuccess)
       return set_error(GDN_EHIP, "verify: LDS attribute: %s", hipGetErrorString(e));
     attr_done = true;
   }
-  hipLaunchKernelGGL((verify_kernel<DK, DV, TIn>), dim3(ns, a.Hv, a.B), dim3(kVT), smem, stream, p);
+  hipLaunchKernelGGL((verify_kernel<DK, DV, TIn>), dim3(ns, a.Hk * (G / hpw), a.B), dim3(kVT), smem,
+                     stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify launch: %s", hipGetErrorString(e));
   return GDN_OK;
