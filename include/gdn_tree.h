@@ -87,7 +87,8 @@ typedef struct {
 #define GDN_MAX_T 128
 
 /* Size in bytes of the tree-metadata blob for B trees of T slots (host only,
- * no device work).  Layout, W = ceil(T/64), all offsets multiples of 8:
+ * no device work).  Layout, W = ceil(T/64); each array starts at the next
+ * 16-byte aligned offset after the previous one, in this order:
  *   uint64 anc   [B][T][W]  bit (j mod 64) of word j/64 of anc[b][i] is set
  *                           iff slot j is a proper ancestor of slot i
  *                           (Sec. 3.4.2 bitmask, node-index space)
@@ -98,8 +99,14 @@ typedef struct {
  *   int32  parent[B][T]     copy of the input parent array
  *   int32  status[B]        GDN_TREE_* code of each tree
  *   int32  nvalid[B]        number of real (non-padding) nodes
- * A tree with a non-zero status gets depth -1, identity order/pos, empty
- * ancestor sets and nvalid 0.  Returns 0 for B <= 0 or T <= 0. */
+ *   int32  pdep  [B][T]     depth of the node at canonical position p
+ *                           (depth[order[p]]), -1 for padding
+ *   int32  ppos  [B][T]     canonical position of the parent of the node at
+ *                           position p (pos[parent[order[p]]]), -1 for the
+ *                           root and padding
+ * The blob is padded to a multiple of 256 bytes.  A tree with a non-zero
+ * status gets depth/pdep/ppos -1, identity order/pos, empty ancestor sets and
+ * nvalid 0.  Returns 0 for B <= 0 or T <= 0. */
 size_t gdn_tree_meta_bytes(int32_t B, int32_t T);
 
 /* Tree preprocessing (Sec. 3.4.1 topological order and ancestor relation,

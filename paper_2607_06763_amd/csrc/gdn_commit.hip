@@ -2,13 +2,17 @@
 // accepted leaf is known a single pass replays Eq. 7 along its path and
 // writes the state; it is the only state write of the decode step).
 //
-// Kernel 1 (grid Hv x B, 256 threads): the path root..a of the accepted slot
-// a is read off its ancestor bitmask; the conv + SiLU + L2-norm features of
-// the path nodes are computed in chunks of kChunk nodes into LDS; each row of
-// S[b][h] (dv rows of dk) lives in the registers of LPR lanes and takes one
-// rank-1 step per path node,
+// Kernel 1 (grid Hv x B, 512 threads): the state loads are issued first; the
+// path root..a of the accepted slot a is read off its ancestor bitmask; each
+// half of the workgroup featurises half of a chunk of kChunk path nodes (one
+// thread per feature channel, width-4 conv window along the path, conv-state
+// slots above the root) into LDS, with the key norms reduced across waves;
+// each row of S[b][h] (dv rows of dk) lives in the registers of LPR lanes and
+// takes one rank-1 step per path node,
 //     S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T,
 // which is Eq. 7 in the stored orientation S <- alpha S (I - beta k k^T) + beta v k^T.
+// The rows are kept as S = gamma * S_stored with gamma the running product of
+// alpha, so a step is two FMAs per element (dot and write).
 // Kernel 2 (grid ceil(C/256) x B) shifts the conv state: the new slots are
 // the last three raw inputs of (old slots | path root..a).  It runs after
 // kernel 1 on the same stream because kernel 1 reads the old conv state.
@@ -16,7 +20,8 @@
 
 namespace gdn {
 
-constexpr int kCT = 256;     // threads per state workgroup
+// threads per state workgroup: 512, or one per state element for tiny heads
+constexpr int commit_threads(int dk, int dv) { return dk * dv >= 512 ? 512 : dk * dv; }
 constexpr int kChunk = 16;   // path nodes featurised per LDS chunk
 constexpr int kCMaxT = 128;  // tree slots supported
 
@@ -42,18 +47,23 @@ __device__ __forceinline__ int commit_check(const MetaPtrs& m, int b, int T, int
 }
 
 template <int DK, int DV, typename TIn>
-__global__ __launch_bounds__(kCT) void commit_state_kernel(CommitParams p) {
-  constexpr int EPT = DV * DK / kCT;       // state elements per thread
-  constexpr int LPR = DK / EPT;            // lanes per state row (power of 2)
-  constexpr int KPL = DK / kWave > 0 ? DK / kWave : 1;  // k channels per lane
-  constexpr int VPL = DV / kWave > 0 ? DV / kWave : 1;  // v channels per lane
+__global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(CommitParams p) {
+  constexpr int kCT = commit_threads(DK, DV);
+  constexpr int EPT = DV * DK / kCT;  // state elements per thread
+  constexpr int LPR = DK / EPT;       // lanes per state row (power of 2)
+  constexpr int NCH = DK + DV;        // feature channels: k of key head g, v of head h
+  constexpr int HALF = kCT / 2;       // threads per feature half
+  constexpr int CPT = (NCH + HALF - 1) / HALF;  // feature channels per thread
+  constexpr int MH = kChunk / 2;      // path nodes per half and chunk
   static_assert(EPT >= 1 && (EPT < 4 || EPT % 4 == 0), "state split");
   static_assert(LPR >= 1 && LPR <= kWave && (LPR & (LPR - 1)) == 0, "row lanes");
 
   __shared__ int s_path[kCMaxT];
+  __shared__ int s_dep[kCMaxT];
   __shared__ float s_al[kCMaxT], s_be[kCMaxT];
-  __shared__ __align__(16) float s_k[kChunk][DK];
-  __shared__ float s_v[kChunk][DV];
+  __shared__ __align__(16) float s_f[kChunk][NCH];  // conv+SiLU features of a path chunk
+  __shared__ float s_part[kChunk][kCT / kWave];     // per-wave partial sums of k^2
+  __shared__ float s_inv[kChunk];                   // 1 / ||k|| per path node
 
   const int h = blockIdx.x, b = blockIdx.y;
   const int T = p.T, Hk = p.Hk, Hv = p.Hv;
@@ -61,30 +71,29 @@ __global__ __launch_bounds__(kCT) void commit_state_kernel(CommitParams p) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int C = 2 * Hk * DK + Hv * DV;
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
-  const int a = p.accepted[b];
-  const int st = commit_check(m, b, T, a);
-  if (h == 0 && tid == 0 && p.commit_status) p.commit_status[b] = st;
-  if (st != GDN_TREE_OK || a == -1) return;
-
-  const int d = m.depth[size_t(b) * T + a];
   const TIn* alpha = static_cast<const TIn*>(p.alpha);
   const TIn* beta = static_cast<const TIn*>(p.beta);
-  for (int j = tid; j < T; j += kCT) {
-    const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (j >> 6)];
-    if (j == a || ((word >> (j & 63)) & 1ull)) {
-      const int dj = m.depth[size_t(b) * T + j];
-      s_path[dj] = j;
-      const size_t ab = (size_t(b) * T + j) * Hv + h;
-      s_al[dj] = ld(alpha, ab);
-      s_be[dj] = ld(beta, ab);
-    }
-  }
 
-  // state rows in registers
+  // first round of loads: nothing here depends on the accepted slot
+  const int a = p.accepted[b];
+  const int tree_st = m.status[b];
+  int dep_j = -1;
+  float al_j = 0.0f, be_j = 0.0f;
+  if (tid < T) {
+    dep_j = m.depth[size_t(b) * T + tid];
+    const size_t ab = (size_t(b) * T + tid) * Hv + h;
+    al_j = ld(alpha, ab);
+    be_j = ld(beta, ab);
+  }
+  if (tree_st != GDN_TREE_OK || a < 0 || a >= T) {
+    if (h == 0 && tid == 0 && p.commit_status)
+      p.commit_status[b] = tree_st != GDN_TREE_OK ? tree_st : (a == -1 ? GDN_TREE_OK : GDN_TREE_BAD_ACCEPTED);
+    return;
+  }
   const int row = tid / LPR;
   const int col0 = (tid % LPR) * EPT;
   float* Sbh = p.S + (size_t(b) * Hv + h) * size_t(DV) * DK;
-  float srow[EPT];
+  float srow[EPT];  // state rows in registers; the loads overlap the path work
   if constexpr (EPT % 4 == 0) {
 #pragma unroll
     for (int e = 0; e < EPT; e += 4) {
@@ -98,101 +107,143 @@ __global__ __launch_bounds__(kCT) void commit_state_kernel(CommitParams p) {
 #pragma unroll
     for (int e = 0; e < EPT; ++e) srow[e] = Sbh[size_t(row) * DK + col0 + e];
   }
+  if (tid < T) s_dep[tid] = dep_j;
   __syncthreads();
+  const int d = s_dep[a];
+  if (h == 0 && tid == 0 && p.commit_status)
+    p.commit_status[b] = d < 0 ? GDN_TREE_BAD_ACCEPTED : GDN_TREE_OK;
+  if (d < 0) return;  // accepted slot is padding
 
+  // second round: the path root..a from the ancestor bitmask of a
+  if (tid < T) {
+    const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (tid >> 6)];
+    if (tid == a || ((word >> (tid & 63)) & 1ull)) {
+      s_path[dep_j] = tid;
+      s_al[dep_j] = al_j;
+      s_be[dep_j] = be_j;
+    }
+  }
+
+  // feature channels of this thread: c < DK -> k[g][c], else v[h][c - DK]
+  const int half = tid / HALF, ht = tid % HALF;
   const TIn* kin = static_cast<const TIn*>(p.k);
   const TIn* vin = static_cast<const TIn*>(p.v);
-  const int kch0 = Hk * DK + g * DK;    // conv channel of k[g][0]
-  const int vch0 = 2 * Hk * DK + h * DV;  // conv channel of v[h][0]
+  const size_t krow = size_t(Hk) * DK, vrow = size_t(Hv) * DV;
+  float wt[CPT][4];
+  const TIn* src[CPT];
+  size_t sstride[CPT];
+  const float* csrc[CPT];
+#pragma unroll
+  for (int u = 0; u < CPT; ++u) {
+    const int c = ht + u * HALF;
+    const int cc = c < NCH ? c : 0;
+    const int ch = cc < DK ? Hk * DK + g * DK + cc : 2 * Hk * DK + h * DV + (cc - DK);
+    src[u] = cc < DK ? kin + size_t(b) * T * krow + size_t(g) * DK + cc
+                     : vin + size_t(b) * T * vrow + size_t(h) * DV + (cc - DK);
+    sstride[u] = cc < DK ? krow : vrow;
+    csrc[u] = p.conv_state + size_t(b) * 3 * C + ch;
+    const float4 w4 = *reinterpret_cast<const float4*>(p.conv_w + size_t(ch) * 4);
+    wt[u][0] = w4.x;
+    wt[u][1] = w4.y;
+    wt[u][2] = w4.z;
+    wt[u][3] = w4.w;
+  }
+  __syncthreads();  // s_path ready
+
+  // S_true = gamma * srow: one step costs one FMA for S.k and one for the
+  // rank-1 write, S_true <- alpha S_true + c k  <=>  srow += c / (alpha gamma) k
+  float gamma = 1.0f;
   for (int base = 0; base <= d; base += kChunk) {
-    // features of path nodes base .. base+kChunk-1: one wave per node
-    for (int mrel = wave; mrel < kChunk; mrel += kCT / kWave) {
-      const int mi = base + mrel;
-      if (mi > d) break;
-      float yk[KPL], yv[VPL];
-      float ss = 0.0f;
+    const int cnt = (d - base + 1) < kChunk ? (d - base + 1) : kChunk;
+    // this half featurises path nodes base + half * MH .. + MH - 1; the
+    // window before its first node comes from the path or the conv state
+    const int m0 = base + half * MH;
+    float ksq[MH];
 #pragma unroll
-      for (int e = 0; e < KPL; ++e) {
-        const int c = lane * KPL + e;
-        float y = 0.0f;
-        if (c < DK) {
+    for (int mr = 0; mr < MH; ++mr) ksq[mr] = 0.0f;
 #pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int mm = mi - 3 + w;
-            const float x = mm >= 0
-                                ? ld(kin, (size_t(b) * T + s_path[mm]) * Hk * DK + size_t(g) * DK + c)
-                                : p.conv_state[(size_t(b) * 3 + (3 + mm)) * C + kch0 + c];
-            y += p.conv_w[size_t(kch0 + c) * 4 + w] * x;
-          }
-          y = silu(y);
-        }
-        yk[e] = y;
-        ss += y * y;
+    for (int u = 0; u < CPT; ++u) {
+      const int c = ht + u * HALF;
+      float xs[MH + 3];
+#pragma unroll
+      for (int q = 0; q < MH + 3; ++q) {
+        const int mi = m0 - 3 + q;  // path index of this window element
+        xs[q] = mi < 0 ? csrc[u][size_t(3 + mi) * C]
+                       : (mi <= d ? ld(src[u], size_t(s_path[mi]) * sstride[u]) : 0.0f);
       }
 #pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) ss += __shfl_xor(ss, o);
-      const float inv = rsqrt_hw(ss + 1e-6f);
-#pragma unroll
-      for (int e = 0; e < KPL; ++e) {
-        const int c = lane * KPL + e;
-        if (c < DK) s_k[mrel][c] = yk[e] * inv;
-      }
-#pragma unroll
-      for (int e = 0; e < VPL; ++e) {
-        const int c = lane * VPL + e;
-        if (c < DV) {
-          float y = 0.0f;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int mm = mi - 3 + w;
-            const float x = mm >= 0
-                                ? ld(vin, (size_t(b) * T + s_path[mm]) * Hv * DV + size_t(h) * DV + c)
-                                : p.conv_state[(size_t(b) * 3 + (3 + mm)) * C + vch0 + c];
-            y += p.conv_w[size_t(vch0 + c) * 4 + w] * x;
-          }
-          yv[e] = silu(y);
-          s_v[mrel][c] = yv[e];
-        }
+      for (int mr = 0; mr < MH; ++mr) {
+        const float y = silu(wt[u][0] * xs[mr] + wt[u][1] * xs[mr + 1] + wt[u][2] * xs[mr + 2] +
+                             wt[u][3] * xs[mr + 3]);
+        if (c < NCH) s_f[half * MH + mr][c] = y;
+        if (c < DK) ksq[mr] += y * y;
       }
     }
+    // ||k||^2 per path node: wave sums, then across the waves of the half
+#pragma unroll
+    for (int mr = 0; mr < MH; ++mr) {
+      float v = ksq[mr];
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o);
+      if (lane == 0) s_part[half * MH + mr][wave % (HALF / kWave)] = v;
+    }
     __syncthreads();
-    const int cnt = (d - base + 1) < kChunk ? (d - base + 1) : kChunk;
-    for (int mrel = 0; mrel < cnt; ++mrel) {
-      const int mi = base + mrel;
-      const float al = s_al[mi], be = s_be[mi];
+    if (tid < kChunk) {
+      float v = 0.0f;
+#pragma unroll
+      for (int wv = 0; wv < HALF / kWave; ++wv) v += s_part[tid][wv];
+      s_inv[tid] = rsqrt_hw(v + 1e-6f);
+    }
+    __syncthreads();
+    for (int mr = 0; mr < cnt; ++mr) {
+      const int mi = base + mr;
+      const float al = s_al[mi], be = s_be[mi], inv = s_inv[mr];
       float kk[EPT];
       if constexpr (EPT % 4 == 0) {
 #pragma unroll
         for (int e = 0; e < EPT; e += 4) {
-          const float4 x = *reinterpret_cast<const float4*>(&s_k[mrel][col0 + e]);
-          kk[e] = x.x;
-          kk[e + 1] = x.y;
-          kk[e + 2] = x.z;
-          kk[e + 3] = x.w;
+          const float4 x = *reinterpret_cast<const float4*>(&s_f[mr][col0 + e]);
+          kk[e] = x.x * inv;
+          kk[e + 1] = x.y * inv;
+          kk[e + 2] = x.z * inv;
+          kk[e + 3] = x.w * inv;
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) kk[e] = s_k[mrel][col0 + e];
+        for (int e = 0; e < EPT; ++e) kk[e] = s_f[mr][col0 + e] * inv;
       }
-      float u = 0.0f;
+      float u0 = 0.0f, u1 = 0.0f;
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) u += srow[e] * kk[e];
+      for (int e = 0; e + 1 < EPT; e += 2) {
+        u0 += srow[e] * kk[e];
+        u1 += srow[e + 1] * kk[e + 1];
+      }
+      if (EPT & 1) u0 += srow[EPT - 1] * kk[EPT - 1];
+      float uu = u0 + u1;
 #pragma unroll
-      for (int o = 1; o < LPR; o <<= 1) u += __shfl_xor(u, o);
-      const float c = be * (s_v[mrel][row] - al * u);
+      for (int o = 1; o < LPR; o <<= 1) uu += __shfl_xor(uu, o);
+      // c = beta (v_r - alpha S_true.k), scaled into the stored frame
+      const float ag = al * gamma;
+      const float c = be * (s_f[mr][DK + row] - ag * uu) * __builtin_amdgcn_rcpf(ag);
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) srow[e] = al * srow[e] + c * kk[e];
+      for (int e = 0; e < EPT; ++e) srow[e] += c * kk[e];
+      gamma = ag;
+      if (gamma < 0x1p-60f) {  // keep the stored frame in range (uniform branch)
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) srow[e] *= gamma;
+        gamma = 1.0f;
+      }
     }
-    __syncthreads();
+    __syncthreads();  // chunk features consumed
   }
   if constexpr (EPT % 4 == 0) {
 #pragma unroll
     for (int e = 0; e < EPT; e += 4)
       *reinterpret_cast<float4*>(Sbh + size_t(row) * DK + col0 + e) =
-          make_float4(srow[e], srow[e + 1], srow[e + 2], srow[e + 3]);
+          make_float4(srow[e] * gamma, srow[e + 1] * gamma, srow[e + 2] * gamma, srow[e + 3] * gamma);
   } else {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) Sbh[size_t(row) * DK + col0 + e] = srow[e];
+    for (int e = 0; e < EPT; ++e) Sbh[size_t(row) * DK + col0 + e] = srow[e] * gamma;
   }
 }
 
@@ -238,7 +289,8 @@ __global__ __launch_bounds__(256) void commit_conv_kernel(CommitParams p, int DK
 
 template <int DK, int DV, typename TIn>
 static int launch_commit_t(const CommitParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((commit_state_kernel<DK, DV, TIn>), dim3(p.Hv, p.B), dim3(kCT), 0, stream, p);
+  hipLaunchKernelGGL((commit_state_kernel<DK, DV, TIn>), dim3(p.Hv, p.B), dim3(commit_threads(DK, DV)), 0,
+                     stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "commit launch: %s", hipGetErrorString(e));
   const int C = 2 * p.Hk * DK + p.Hv * DV;

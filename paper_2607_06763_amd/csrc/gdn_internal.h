@@ -22,7 +22,7 @@ constexpr int kRoot = -1;  // parent value of the root
 // a 16-byte aligned offset.
 // ---------------------------------------------------------------------------
 struct MetaLayout {
-  size_t anc, depth, order, pos, parent, status, nvalid, total;
+  size_t anc, depth, order, pos, parent, status, nvalid, pdep, ppos, total;
   int W;
 };
 
@@ -39,7 +39,9 @@ __host__ __device__ inline MetaLayout meta_layout(int B, int T) {
   m.parent = align16(m.pos + 4 * bt);
   m.status = align16(m.parent + 4 * bt);
   m.nvalid = align16(m.status + 4 * size_t(B));
-  size_t end = m.nvalid + 4 * size_t(B);
+  m.pdep = align16(m.nvalid + 4 * size_t(B));
+  m.ppos = align16(m.pdep + 4 * bt);
+  size_t end = m.ppos + 4 * bt;
   m.total = (end + 255) & ~size_t(255);
   return m;
 }
@@ -52,6 +54,8 @@ struct MetaPtrs {
   int32_t* parent;
   int32_t* status;
   int32_t* nvalid;
+  int32_t* pdep;
+  int32_t* ppos;
   int W;
 };
 
@@ -66,6 +70,8 @@ __host__ __device__ inline MetaPtrs meta_ptrs(const void* base, int B, int T) {
   m.parent = (int32_t*)(p + l.parent);
   m.status = (int32_t*)(p + l.status);
   m.nvalid = (int32_t*)(p + l.nvalid);
+  m.pdep = (int32_t*)(p + l.pdep);
+  m.ppos = (int32_t*)(p + l.ppos);
   m.W = l.W;
   return m;
 }

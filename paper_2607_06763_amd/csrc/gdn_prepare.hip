@@ -98,6 +98,8 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
       m.order[base + i] = i;
       m.pos[base + i] = i;
       m.parent[base + i] = p;
+      m.pdep[base + i] = -1;
+      m.ppos[base + i] = -1;
       for (int w = 0; w < W; ++w) m.anc[(size_t(base) + i) * W + w] = 0;
     }
     if (i == 0) {
@@ -123,6 +125,13 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
     m.depth[base + i] = real ? dep : -1;
     m.parent[base + i] = p;
     for (int w = 0; w < W; ++w) m.anc[(size_t(base) + i) * W + w] = real ? anc[w] : 0;
+    s_nxt[i] = rank;  // position of slot i (s_nxt is free after the jumps)
+  }
+  __syncthreads();
+  if (slot) {  // per-position copies: depth and parent position
+    const int rank = s_nxt[i];
+    m.pdep[base + rank] = real ? dep : -1;
+    m.ppos[base + rank] = (real && p >= 0) ? s_nxt[p] : -1;
   }
   if (i == 0) {
     m.status[b] = GDN_TREE_OK;

@@ -227,6 +227,8 @@ def meta_layout(B: int, T: int) -> dict:
     off["parent"] = a16(off["pos"] + 4 * B * T)
     off["status"] = a16(off["parent"] + 4 * B * T)
     off["nvalid"] = a16(off["status"] + 4 * B)
+    off["pdep"] = a16(off["nvalid"] + 4 * B)
+    off["ppos"] = a16(off["pdep"] + 4 * B * T)
     off["W"] = W
     return off
 
@@ -244,4 +246,6 @@ def unpack_meta(raw, B: int, T: int) -> dict:
                 pos=arr("pos", np.int32, B * T, (B, T)),
                 parent=arr("parent", np.int32, B * T, (B, T)),
                 status=arr("status", np.int32, B, (B,)),
-                nvalid=arr("nvalid", np.int32, B, (B,)))
+                nvalid=arr("nvalid", np.int32, B, (B,)),
+                pdep=arr("pdep", np.int32, B * T, (B, T)),
+                ppos=arr("ppos", np.int32, B * T, (B, T)))

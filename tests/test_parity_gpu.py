@@ -40,6 +40,18 @@ def _check_meta(G, dt, w, orc):
     if ok.any():
         pos = np.argsort(ref["order"], axis=1)
         np.testing.assert_array_equal(got["pos"][ok], pos[ok])
+    # per-position copies: depth of the node at position p, parent's position
+    B, T = w.parent.shape
+    for b in range(B):
+        if ref["status"][b] != 0:
+            assert (got["pdep"][b] == -1).all() and (got["ppos"][b] == -1).all()
+            continue
+        pos = np.argsort(ref["order"][b])
+        for p_ in range(T):
+            node = ref["order"][b, p_]
+            assert got["pdep"][b, p_] == ref["depth"][b, node]
+            par = w.parent[b, node]
+            assert got["ppos"][b, p_] == (pos[par] if par >= 0 else -1)
     np.testing.assert_array_equal(got["parent"], w.parent)
     np.testing.assert_array_equal(dt.tree_status.cpu().numpy(), ref["status"])
 
