@@ -56,7 +56,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
   constexpr int CPT = (NCH + HALF - 1) / HALF;  // feature channels per thread
   constexpr int MH = kChunk / 2;      // path nodes per half and chunk
   static_assert(EPT >= 1 && (EPT < 4 || EPT % 4 == 0), "state split");
-  static_assert(LPR >= 1 && LPR <= kWave && (LPR & (LPR - 1)) == 0, "row lanes");
+  static_assert(LPR >= 1 && LPR <= 32 && (LPR & (LPR - 1)) == 0, "row lanes");
 
   __shared__ int s_path[kCMaxT];
   __shared__ int s_dep[kCMaxT];
@@ -182,9 +182,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
     // ||k||^2 per path node: wave sums, then across the waves of the half
 #pragma unroll
     for (int mr = 0; mr < MH; ++mr) {
-      float v = ksq[mr];
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) v += __shfl_xor(v, o);
+      const float v = wave_sum(ksq[mr]);
       if (lane == 0) s_part[half * MH + mr][wave % (HALF / kWave)] = v;
     }
     __syncthreads();
@@ -198,19 +196,19 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
     for (int mr = 0; mr < cnt; ++mr) {
       const int mi = base + mr;
       const float al = s_al[mi], be = s_be[mi], inv = s_inv[mr];
-      float kk[EPT];
+      float kk[EPT];  // un-normalised key; 1 / ||k|| is folded into the scalars
       if constexpr (EPT % 4 == 0) {
 #pragma unroll
         for (int e = 0; e < EPT; e += 4) {
           const float4 x = *reinterpret_cast<const float4*>(&s_f[mr][col0 + e]);
-          kk[e] = x.x * inv;
-          kk[e + 1] = x.y * inv;
-          kk[e + 2] = x.z * inv;
-          kk[e + 3] = x.w * inv;
+          kk[e] = x.x;
+          kk[e + 1] = x.y;
+          kk[e + 2] = x.z;
+          kk[e + 3] = x.w;
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) kk[e] = s_f[mr][col0 + e] * inv;
+        for (int e = 0; e < EPT; ++e) kk[e] = s_f[mr][col0 + e];
       }
       float u0 = 0.0f, u1 = 0.0f;
 #pragma unroll
@@ -219,12 +217,11 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
         u1 += srow[e + 1] * kk[e + 1];
       }
       if (EPT & 1) u0 += srow[EPT - 1] * kk[EPT - 1];
-      float uu = u0 + u1;
-#pragma unroll
-      for (int o = 1; o < LPR; o <<= 1) uu += __shfl_xor(uu, o);
-      // c = beta (v_r - alpha S_true.k), scaled into the stored frame
+      const float uu = group_sum<LPR>(u0 + u1) * inv;  // S_stored . k_hat
+      // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
+      // multiplied by 1 / ||k|| so that it applies to the raw key
       const float ag = al * gamma;
-      const float c = be * (s_f[mr][DK + row] - ag * uu) * __builtin_amdgcn_rcpf(ag);
+      const float c = be * (s_f[mr][DK + row] - ag * uu) * __builtin_amdgcn_rcpf(ag) * inv;
 #pragma unroll
       for (int e = 0; e < EPT; ++e) srow[e] += c * kk[e];
       gamma = ag;

@@ -111,6 +111,40 @@ __device__ __forceinline__ float silu(float y) {
 __device__ __forceinline__ float rsqrt_hw(float x) { return __builtin_amdgcn_rsqf(x); }
 
 // ---------------------------------------------------------------------------
+// Cross-lane sums with DPP (VALU-rate, no LDS round trip).
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppQuadXor1 = 0xB1;      // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
+constexpr int kDppRowHalfMirror = 0x141;  // lane i <-> 7-i within each 8 lanes
+constexpr int kDppRowMirror = 0x140;      // lane i <-> 15-i within each 16 lanes
+
+// Sum over aligned groups of N consecutive lanes (N = 1, 2, ..., 32); every
+// lane of a group receives the group's sum.  Up to 16 lanes this is DPP only;
+// the step across 16-lane rows goes through ds_bpermute.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16 || N == 32, "group size");
+  if constexpr (N >= 2) v += dpp_f<kDppQuadXor1>(v);
+  if constexpr (N >= 4) v += dpp_f<kDppQuadXor2>(v);
+  if constexpr (N >= 8) v += dpp_f<kDppRowHalfMirror>(v);
+  if constexpr (N >= 16) v += dpp_f<kDppRowMirror>(v);
+  if constexpr (N >= 32) v += __shfl_xor(v, 16);
+  return v;
+}
+
+// Sum over the whole wave (64 lanes), returned in every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum<16>(v);
+  const int b = __float_as_int(v);
+  return __int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16)) +
+         __int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48));
+}
+
+// ---------------------------------------------------------------------------
 // Launchers (defined in the kernel sources).  All return a gdn_status value.
 // ---------------------------------------------------------------------------
 int launch_prepare(int B, int T, const int32_t* parent, void* meta, int32_t* tree_status,
