@@ -20,21 +20,28 @@
 // ~1e-5 relative error).
 //
 // Workgroup = (dv slice, key head g with HPW of its value heads, sequence b),
-// 512 threads.  Wave w owns the 16 tree positions [16w, 16w+16) of the
-// canonical (depth, index) order; lane (l16, lg) of a wave holds, for node
-// 16w + l16, the key channels 32kb + 8lg + e and the value channels
-// 16n + 4lg + e.  That is exactly the MFMA B-operand layout of X~^T and the
-// accumulator layout of O^T for v_mfma_f32_16x16x32_bf16, so the pulled-back
-// queries and the value accumulators never leave registers.
+// 512 threads.  Wave w owns 16 tree positions of the canonical (depth,
+// index) order: 8 from a shallow block of 16 and 8 from a deep one, so that
+// all waves walk about equally long paths.  Two layouts are used:
+//   * conv / pull-back: 8 lanes per node, lane (n, o) = (lane / 8, lane % 8)
+//     carries shallow node n and deep node n of the wave (walked one after
+//     the other) and the channels lane_chan(o, r); a node's 8 lanes read 128
+//     contiguous bytes of an LDS row per access, which keeps bank conflicts
+//     low when the 8 nodes of a wave read 8 unrelated ancestor rows;
+//   * MFMA: node column l16 = lane % 16, lane group mlg = lane / 16, the
+//     B-operand layout of X~^T and the accumulator layout of O^T for
+//     v_mfma_f32_16x16x32_bf16.  One ds_bpermute per register and node half
+//     moves the pulled-back queries and value accumulators across.
 //   phase 0  tree metadata in canonical order -> LDS; prefetch S0 and raw v
 //            of the first head into registers
 //   phase 1  conv + SiLU + L2-norm of q and k along each node's path (raw
 //            rows staged in LDS); q~ stays in registers, k~ -> LDS (fp32)
 //   per value head:
-//     2a/b   raw v -> LDS, conv + SiLU -> v~ in LDS (fp32); prefetch the next
-//            head's raw v
-//     2c     pull-back with k~, v~ gathered from LDS (4 lanes per node)
-//     2d     S0 (prefetched) -> LDS as bf16 hi/lo planes; prefetch next S0
+//     2a/b   raw v (prefetched) -> LDS, conv + SiLU -> v~ in LDS (fp32)
+//     2c     pull-back with k~, v~ gathered from LDS (8 lanes per node),
+//            move to the MFMA layout
+//     2d     S0 (prefetched) -> LDS as bf16 hi/lo planes; prefetch the next
+//            head's S0, raw v, gates and v conv weights
 //     2e     MFMA O^T = S0 X~^T + ACC^T, store
 #include "gdn_internal.h"
 
@@ -48,6 +55,7 @@ constexpr int kVT = 512;        // threads per workgroup (8 waves)
 constexpr int kVMaxT = 128;     // tree slots supported = 8 waves x 16 nodes
 constexpr int kKPad = 4;        // fp32 row padding of the k~ and v~ tiles
 constexpr int kSPad = 8;        // bf16 row padding of the S0 planes
+constexpr int kLPN = 8;         // lanes per node in the conv / pull-back layout
 
 struct VerifyParams {
   int B, T, Hk, Hv, DV, hpw;
@@ -57,6 +65,71 @@ struct VerifyParams {
   const float *conv_w, *conv_state, *S0;
   float* out;
 };
+
+// Channel carried in register r (r < D / 8) by lane o (o < 8) of a node:
+// groups of 4 consecutive channels, lane o taking group o of every 32.
+template <int D>
+__device__ __forceinline__ constexpr int lane_chan(int o, int r) {
+  return D >= 32 ? 32 * (r / 4) + 4 * o + (r % 4) : 2 * o + r;
+}
+
+// This lane's D / 8 channels of an fp32 LDS row (16-byte or 8-byte pieces).
+template <int D>
+__device__ __forceinline__ void ld_lane(const float* row, int o, float (&x)[D / kLPN]) {
+  if constexpr (D >= 32) {
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) {
+      const float4 v = *reinterpret_cast<const float4*>(row + 32 * c + 4 * o);
+      x[4 * c] = v.x;
+      x[4 * c + 1] = v.y;
+      x[4 * c + 2] = v.z;
+      x[4 * c + 3] = v.w;
+    }
+  } else {
+    const float2 v = *reinterpret_cast<const float2*>(row + 2 * o);
+    x[0] = v.x;
+    x[1] = v.y;
+  }
+}
+template <int D>
+__device__ __forceinline__ void st_lane(float* row, int o, const float (&x)[D / kLPN]) {
+  if constexpr (D >= 32) {
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c)
+      *reinterpret_cast<float4*>(row + 32 * c + 4 * o) =
+          make_float4(x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]);
+  } else {
+    *reinterpret_cast<float2*>(row + 2 * o) = make_float2(x[0], x[1]);
+  }
+}
+
+// Staged rows read by the four conv taps of the nodes at positions pos[u]:
+// tap w of a node at depth d is its path node at depth d - 3 + w, or
+// conv-state row T + d + w (slot d + w) above the root.  Inactive -> row 0.
+__device__ __forceinline__ void conv_rows(const int* s_dep, const int* s_ppos, int T, const int (&pos)[2],
+                                          const bool (&act)[2], int (&trow)[2][4]) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) trow[u][w] = 0;
+    if (act[u]) {
+      const int dep = s_dep[pos[u]];
+      const int t2 = s_ppos[pos[u]];
+      const int t1 = t2 >= 0 ? s_ppos[t2] : -1;
+      const int t0 = t1 >= 0 ? s_ppos[t1] : -1;
+      const int tp[4] = {t0, t1, t2, pos[u]};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) trow[u][w] = (dep - 3 + w >= 0) ? tp[w] : T + dep + w;
+    }
+  }
+}
+
+// Offset (floats) of row t of a tile with rows of D + kKPad floats.
+template <int D>
+__device__ __forceinline__ int row_off(int t) {
+  static_assert((D & (D - 1)) == 0 && kKPad == 4, "power-of-two rows plus 4");
+  return (t << __builtin_ctz(D)) + (t << 2);
+}
 
 // bf16 hi/lo split by truncation: x = hi + lo + O(2^-16 |x|).
 __device__ __forceinline__ void split8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
@@ -96,30 +169,10 @@ __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const
   return c;
 }
 
-// 8 consecutive input elements as floats (16 B for bf16, 32 B for fp32)
-__device__ __forceinline__ void ld8(const float* p, float (&x)[8]) {
-  const float4 a = *reinterpret_cast<const float4*>(p);
-  const float4 b = *reinterpret_cast<const float4*>(p + 4);
-  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-}
-__device__ __forceinline__ void ld8(const BF16* p, float (&x)[8]) {
-  const uint4 u = *reinterpret_cast<const uint4*>(p);
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    x[2 * e] = __uint_as_float(w[e] << 16);
-    x[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
-  }
-}
-
-
-// Sum over the 4 lanes of a quad (DPP quad permutations, no LDS traffic).
-__device__ __forceinline__ float quad_sum(float v) {
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));  // [1,0,3,2]
-  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));  // [2,3,0,1]
-  return v;
-}
+// Pins x to a register at this point: keeps the compiler from sinking the
+// arithmetic that produces it past a later barrier (which would keep every
+// operand it reads alive across the barrier).
+__device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
 // Value of v held by lane src of this wave (ds_bpermute).
 __device__ __forceinline__ float lane_gather(float v, int src) {
@@ -169,11 +222,56 @@ __device__ __forceinline__ void prefetch_v(const TIn* vin, size_t node_stride, c
 #pragma unroll
   for (int j = 0; j < NVC; ++j) {
     const int idx = j * kVT + tid;
-    const int p = idx / CPR, c = idx % CPR;
-    pf[j] = p < T ? *reinterpret_cast<const uint4*>(vin + size_t(s_ord[p]) * node_stride + c * EPC)
-                  : make_uint4(0, 0, 0, 0);
+    const int p = idx / CPR < T ? idx / CPR : T - 1, c = idx % CPR;  // rows >= T are never stored
+    pf[j] = *reinterpret_cast<const uint4*>(vin + size_t(s_ord[p]) * node_stride + c * EPC);
   }
 }
+
+// Gates (alpha, beta of the T positions), v conv weights ([4][DVS],
+// tap-major) and v conv-state rows ([3][DVS]) of one value head, loaded
+// into registers ahead of their use.  Every load is unconditional (indices
+// are clamped) so that nothing waits for it before the store.
+template <int DVS, typename TIn>
+struct HeadGates {
+  static constexpr int NW = (4 * DVS + kVT - 1) / kVT;
+  static constexpr int NC = (3 * DVS + kVT - 1) / kVT;
+  TIn al, be;
+  float w[NW], cs[NC];
+  __device__ __forceinline__ void load(const TIn* alpha, const TIn* beta, const float* conv_w,
+                                       const float* conv_state, const int* s_ord, int b, int T, int Hv,
+                                       int C, int h, int vch0, int tid) {
+    const size_t ab = (size_t(b) * T + s_ord[tid < T ? tid : 0]) * Hv + h;
+    al = alpha[ab];
+    be = beta[ab];
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      const int i = j * kVT + tid < 4 * DVS ? j * kVT + tid : 4 * DVS - 1;
+      w[j] = conv_w[size_t(vch0 + i % DVS) * 4 + i / DVS];
+    }
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const int i = j * kVT + tid < 3 * DVS ? j * kVT + tid : 3 * DVS - 1;
+      cs[j] = conv_state[(size_t(b) * 3 + i / DVS) * C + vch0 + i % DVS];
+    }
+  }
+  // gates -> s_al, s_be; weights -> s_wv; conv-state rows -> rows T..T+2 of
+  // the v staging tile
+  __device__ __forceinline__ void store(float* s_al, float* s_be, float* s_wv, float* s_v, int vrow, int T,
+                                        int tid) const {
+    if (tid < T) {
+      s_al[tid] = to_f32(al);
+      s_be[tid] = to_f32(be);
+    }
+#pragma unroll
+    for (int j = 0; j < NW; ++j)
+      if (j * kVT + tid < 4 * DVS) s_wv[j * kVT + tid] = w[j];
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const int i = j * kVT + tid;
+      if (i < 3 * DVS) s_v[(T + i / DVS) * vrow + i % DVS] = cs[j];
+    }
+  }
+};
 
 // Write one 16-byte chunk of raw inputs (8 bf16 or 4 fp32) to LDS as fp32.
 __device__ __forceinline__ void store_chunk_f32(float* dst, uint4 u, const BF16*) {
@@ -190,7 +288,8 @@ __device__ __forceinline__ void store_chunk_f32(float* dst, uint4 u, const float
 template <int DK, int DVS, typename TIn>
 __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   extern __shared__ __align__(16) unsigned char smem[];
-  constexpr int KPL = DK / 4;                 // key channels per lane: 16 j + 4 lg + e
+  constexpr int KPL = DK / kLPN;              // key channels per lane and node
+  constexpr int VPL = DVS / kLPN;             // value channels per lane and node
   constexpr int KB = DK >= 32 ? DK / 32 : 1;  // 32-wide MFMA k blocks (dk = 16 is zero-padded)
   constexpr int KAPPA = 32 * KB;              // MFMA k extent
   constexpr int KROW = DK + kKPad;            // k~ / staging row stride (floats)
@@ -214,12 +313,19 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   const int C = 2 * Hk * DK + Hv * DV;
   const size_t orow = size_t(Hv) * DV;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // quad layout (conv, pull-back): node = 16 wave + lane / 4, channel group lg = lane % 4
-  const int qlg = lane & 3;
-  const int pos = wave * 16 + (lane >> 2);
-  // MFMA layout (product, store): node = 16 wave + lane % 16, channel group = lane / 16
+  // Positions are sorted by depth, so path lengths grow with the position.
+  // Wave w takes the even (w < 4) or odd (w >= 4) positions of the shallow
+  // block w % 4 and of the deep block 7 - w % 4: every wave then walks about
+  // the same number of steps in total.
+  const int pw = wave & 3, hw = wave >> 2;
+  const int base[2] = {16 * pw + hw, 16 * (7 - pw) + hw};
+  // conv / pull-back layout: node n = lane / 8 of each half, lane o = lane % 8
+  const int ln = lane >> 3, lo = lane & 7;
+  const int pos[2] = {base[0] + 2 * ln, base[1] + 2 * ln};
+  // MFMA layout: node column l16 (l16 < 8 from the shallow half, else the
+  // deep one), channel group mlg
   const int l16 = lane & 15, mlg = lane >> 4;
-  const int mpos = wave * 16 + l16;
+  const int mpos = l16 < 8 ? base[0] + 2 * l16 : base[1] + 2 * (l16 - 8);
 
   const VerifySmem L = verify_smem(T, DK, DVS);
   float* s_k = reinterpret_cast<float*>(smem);  // q staging, then k~ [TP][KROW]
@@ -258,12 +364,13 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     const int part = i / (4 * DK), w = (i / DK) & 3, c = i % DK;
     s_wqk[i] = p.conv_w[size_t(part * Hk * DK + g * DK + c) * 4 + w];
   }
-  float4 s0pf[NS0];
-  prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
   __syncthreads();
   const TIn* vin = static_cast<const TIn*>(p.v);
+  const TIn* alpha = static_cast<const TIn*>(p.alpha);
+  const TIn* beta = static_cast<const TIn*>(p.beta);
+  float4 s0pf[NS0];
   uint4 vpf[NVC];
-  prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, tid, vpf);
+  HeadGates<DVS, TIn> gpf;
 
   // ---------------- phase 1: q~ and k~ ----------------
   // Raw rows are staged in LDS as fp32, in canonical order, followed by the
@@ -287,6 +394,20 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
     }
     float* s_kst = reinterpret_cast<float*>(s_rv);
+    const float* csq = p.conv_state + size_t(b) * 3 * C + g * DK;
+    constexpr int NQS = (3 * DK + kVT - 1) / kVT;
+    float cq[NQS], ck[NQS];
+#pragma unroll
+    for (int j = 0; j < NQS; ++j) {
+      const int i = j * kVT + tid < 3 * DK ? j * kVT + tid : 3 * DK - 1;
+      cq[j] = csq[size_t(i / DK) * C + i % DK];
+      ck[j] = csq[size_t(i / DK) * C + Hk * DK + i % DK];
+    }
+    // the first head's inputs load while q and k are staged: raw v, gates,
+    // conv state, then S0 (issued last, waited for last)
+    prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, tid, vpf);
+    gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid);
+    prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
 #pragma unroll
     for (int j = 0; j < NQC; ++j) {
       const int idx = j * kVT + tid;
@@ -296,77 +417,76 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         store_chunk_f32(s_kst + row * KROW + c, kpf[j], static_cast<const TIn*>(nullptr));
       }
     }
-    const float* csq = p.conv_state + size_t(b) * 3 * C + g * DK;
-    for (int i = tid; i < 3 * DK; i += kVT) {
-      const int sl = i / DK, c = i % DK;
-      s_k[(T + sl) * KROW + c] = csq[size_t(sl) * C + c];
-      s_kst[(T + sl) * KROW + c] = csq[size_t(sl) * C + Hk * DK + c];
+#pragma unroll
+    for (int j = 0; j < NQS; ++j) {
+      const int i = j * kVT + tid;
+      if (i < 3 * DK) {
+        s_k[(T + i / DK) * KROW + i % DK] = cq[j];
+        s_kst[(T + i / DK) * KROW + i % DK] = ck[j];
+      }
     }
   }
   __syncthreads();
-  const bool active = pos < nv;
-  int trow[4] = {0, 0, 0, 0};
-  if (active) {
-    const int dep = s_dep[pos];
-    const int t2 = s_ppos[pos];
-    const int t1 = t2 >= 0 ? s_ppos[t2] : -1;
-    const int t0 = t1 >= 0 ? s_ppos[t1] : -1;
-    const int tp[4] = {t0, t1, t2, pos};
+  bool act[2];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) trow[w] = (dep - 3 + w >= 0) ? tp[w] : T + dep + w;
-  }
-  float qh[KPL];  // q~ of this lane's node (channels 16 j + 4 lg + e)
-  float kh[KPL];
+  for (int u = 0; u < 2; ++u) act[u] = pos[u] < nv;
+  int trow[2][4];
+  conv_rows(s_dep, s_ppos, T, pos, act, trow);
+  float qh[2][KPL];  // q~ of this lane's two nodes (channels lane_chan(lo, r))
+  float kh[2][KPL];
 #pragma unroll
   for (int part = 0; part < 2; ++part) {
     const float* stage = part == 0 ? s_k : reinterpret_cast<const float*>(s_rv);
-    float y[KPL];
+    const float* wpart = s_wqk + part * 4 * DK;
+    float y[2][KPL];
 #pragma unroll
-    for (int c = 0; c < KPL; ++c) y[c] = 0.0f;
-    if (active) {
-      const float* wpart = s_wqk + part * 4 * DK;
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int j = 0; j < DK / 16; ++j) {
-        const int c = 16 * j + 4 * qlg;
+      for (int c = 0; c < KPL; ++c) y[u][c] = 0.0f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float4 x = *reinterpret_cast<const float4*>(stage + trow[w] * KROW + c);
-          const float4 wt = *reinterpret_cast<const float4*>(wpart + w * DK + c);
-          y[4 * j] += wt.x * x.x;
-          y[4 * j + 1] += wt.y * x.y;
-          y[4 * j + 2] += wt.z * x.z;
-          y[4 * j + 3] += wt.w * x.w;
+    for (int w = 0; w < 4; ++w) {
+      float wt[KPL];
+      ld_lane<DK>(wpart + w * DK, lo, wt);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        float xw[KPL];
+        ld_lane<DK>(stage + trow[u][w] * KROW, lo, xw);
+#pragma unroll
+        for (int c = 0; c < KPL; ++c) y[u][c] += wt[c] * xw[c];
+      }
+      __builtin_amdgcn_sched_barrier(0);  // one tap's rows in flight at a time
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      float ss = 0.0f;
+#pragma unroll
+      for (int c = 0; c < KPL; ++c) {
+        y[u][c] = silu(y[u][c]);
+        ss += y[u][c] * y[u][c];
+      }
+      ss = group_sum<kLPN>(ss);
+      const float inv = act[u] ? rsqrt_hw(ss + 1e-6f) : 0.0f;
+#pragma unroll
+      for (int c = 0; c < KPL; ++c) {
+        if (part == 0) {
+          qh[u][c] = y[u][c] * inv;
+        } else {
+          kh[u][c] = y[u][c] * inv;
+          pin(kh[u][c]);
         }
       }
     }
-    float ss = 0.0f;
-#pragma unroll
-    for (int c = 0; c < KPL; ++c) {
-      y[c] = silu(y[c]);
-      ss += y[c] * y[c];
-    }
-    ss = quad_sum(ss);
-    const float inv = rsqrt_hw(ss + 1e-6f);
-#pragma unroll
-    for (int c = 0; c < KPL; ++c) {
-      if (part == 0)
-        qh[c] = active ? y[c] * inv : 0.0f;
-      else
-        kh[c] = active ? y[c] * inv : 0.0f;
-    }
   }
   __syncthreads();  // staged rows consumed
-  if (active) {
 #pragma unroll
-    for (int j = 0; j < DK / 16; ++j)
-      *reinterpret_cast<float4*>(s_k + pos * KROW + 16 * j + 4 * qlg) =
-          make_float4(kh[4 * j], kh[4 * j + 1], kh[4 * j + 2], kh[4 * j + 3]);
-  }
+  for (int u = 0; u < 2; ++u)
+    if (act[u]) st_lane<DK>(s_k + pos[u] * KROW, lo, kh[u]);
 
   // ---------------- phase 2: one value head at a time ----------------
-  const TIn* alpha = static_cast<const TIn*>(p.alpha);
-  const TIn* beta = static_cast<const TIn*>(p.beta);
-  const int src_lane = 4 * l16 + mlg;  // quad-layout lane holding this MFMA lane's data
+  // MFMA lane (l16, mlg) takes node l16 from half l16 / 8 of the 8-lane
+  // group starting at lane sbase
+  const int mhalf = l16 >> 3;
+  const int sbase = kLPN * (l16 & 7);
   for (int hh = 0; hh < p.hpw; ++hh) {
     const int h = h0 + hh;
     // 2a: raw v rows (prefetched) + 3 conv-state rows -> LDS as fp32
@@ -382,107 +502,131 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
           store_chunk_f32(s_v + row * VROW + c, vpf[j], static_cast<const TIn*>(nullptr));
         }
       }
-      const float* cs = p.conv_state + size_t(b) * 3 * C + vch0;
-      for (int i = tid; i < 3 * DVS; i += kVT)
-        s_v[(T + i / DVS) * VROW + i % DVS] = cs[size_t(i / DVS) * C + i % DVS];
     }
-    if (tid < T) {
-      const size_t ab = (size_t(b) * T + s_ord[tid]) * Hv + h;
-      s_al[tid] = ld(alpha, ab);
-      s_be[tid] = ld(beta, ab);
-    }
-    for (int i = tid; i < 4 * DVS; i += kVT)
-      s_wv[i] = p.conv_w[size_t(vch0 + i % DVS) * 4 + i / DVS];
+    gpf.store(s_al, s_be, s_wv, s_v, VROW, T, tid);
     __syncthreads();
-    // 2b: v~ for this lane's node and value channels 16 n + 4 lg + e
-    float vt[4 * NT];
+    // 2b: v~ of this lane's two nodes, channels lane_chan(lo, r)
+    float vt[2][VPL];
+    {
+      int trow[2][4];  // recomputed per head: fewer registers held across heads
+      conv_rows(s_dep, s_ppos, T, pos, act, trow);
 #pragma unroll
-    for (int n = 0; n < NT; ++n) {
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) vt[4 * n + e] = 0.0f;
-      if (active) {
-        const int c = 16 * n + 4 * qlg;
-        float y[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < VPL; ++c) vt[u][c] = 0.0f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          const float4 x = *reinterpret_cast<const float4*>(s_v + trow[w] * VROW + c);
-          const float4 wt = *reinterpret_cast<const float4*>(s_wv + w * DVS + c);
-          y[0] += wt.x * x.x;
-          y[1] += wt.y * x.y;
-          y[2] += wt.z * x.z;
-          y[3] += wt.w * x.w;
+      for (int w = 0; w < 4; ++w) {
+        float wt[VPL];
+        ld_lane<DVS>(s_wv + w * DVS, lo, wt);
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          float xw[VPL];
+          ld_lane<DVS>(s_v + trow[u][w] * VROW, lo, xw);
+#pragma unroll
+          for (int c = 0; c < VPL; ++c) vt[u][c] += wt[c] * xw[c];
         }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) vt[4 * n + e] = silu(y[e]);
+        __builtin_amdgcn_sched_barrier(0);  // one tap's rows in flight at a time
       }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int c = 0; c < VPL; ++c) {
+          vt[u][c] = silu(vt[u][c]);
+          pin(vt[u][c]);
+        }
     }
     __syncthreads();  // staged rows consumed
-    if (active) {
 #pragma unroll
-      for (int n = 0; n < NT; ++n)
-          *reinterpret_cast<float4*>(s_v + pos * VROW + 16 * n + 4 * qlg) =
-              make_float4(vt[4 * n], vt[4 * n + 1], vt[4 * n + 2], vt[4 * n + 3]);
-    }
-    if (hh + 1 < p.hpw)
-      prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
+    for (int u = 0; u < 2; ++u)
+      if (act[u]) st_lane<DVS>(s_v + pos[u] * VROW, lo, vt[u]);
     __syncthreads();
 
-    // 2c: query pull-back along the path, leaf to root (quad layout)
-    float x[KPL];
-    float acc[4 * NT];
+    // 2c: query pull-back along the path of each node, leaf to root; the
+    //     lane walks its shallow node, then its deep one
+    float x[2][KPL], acc[2][VPL];
 #pragma unroll
-    for (int c = 0; c < KPL; ++c) x[c] = qh[c];
+    for (int u = 0; u < 2; ++u) {
 #pragma unroll
-    for (int c = 0; c < 4 * NT; ++c) acc[c] = 0.0f;
-    float r = 1.0f;
-    {
-      int t = active ? pos : -1;
+      for (int c = 0; c < KPL; ++c) x[u][c] = qh[u][c];
+#pragma unroll
+      for (int c = 0; c < VPL; ++c) acc[u][c] = 0.0f;
+      float r = 1.0f;
+      int t = act[u] ? pos[u] : -1;
       // a path has at most T nodes; the bound also ends the walk on corrupt metadata
       for (int step = 0; step < T && t >= 0; ++step) {
-        float kt[KPL];
-#pragma unroll
-        for (int j = 0; j < DK / 16; ++j) {
-          const float4 k4 = *reinterpret_cast<const float4*>(s_k + t * KROW + 16 * j + 4 * qlg);
-          kt[4 * j] = k4.x;
-          kt[4 * j + 1] = k4.y;
-          kt[4 * j + 2] = k4.z;
-          kt[4 * j + 3] = k4.w;
-        }
+        const float be = s_be[t];
+        const float al = s_al[t];
+        const int nx = s_ppos[t];
+        float kt[KPL], vv[VPL];
+        ld_lane<DK>(s_k + row_off<DK>(t), lo, kt);
+        ld_lane<DVS>(s_v + row_off<DVS>(t), lo, vv);
         float s0 = 0.f, s1 = 0.f;
 #pragma unroll
         for (int c = 0; c < KPL; c += 2) {
-          s0 += kt[c] * x[c];
-          s1 += kt[c + 1] * x[c + 1];
+          s0 += kt[c] * x[u][c];
+          s1 += kt[c + 1] * x[u][c + 1];
         }
-        const float s = quad_sum(s0 + s1);
-        const float bs = s_be[t] * s;
+        const float bs = be * group_sum<kLPN>(s0 + s1);
         const float rbs = r * bs;
 #pragma unroll
-        for (int c = 0; c < KPL; ++c) x[c] -= bs * kt[c];
+        for (int c = 0; c < KPL; ++c) x[u][c] -= bs * kt[c];
 #pragma unroll
-        for (int n = 0; n < NT; ++n) {
-          const float4 v4 = *reinterpret_cast<const float4*>(s_v + t * VROW + 16 * n + 4 * qlg);
-          acc[4 * n] += rbs * v4.x;
-          acc[4 * n + 1] += rbs * v4.y;
-          acc[4 * n + 2] += rbs * v4.z;
-          acc[4 * n + 3] += rbs * v4.w;
-        }
-        r *= s_al[t];
-        t = s_ppos[t];
+        for (int c = 0; c < VPL; ++c) acc[u][c] += rbs * vv[c];
+        r *= al;
+        t = nx;
       }
+#pragma unroll
+      for (int c = 0; c < KPL; ++c) x[u][c] *= r;
     }
-    // a_i x~_i and the value accumulators move from the quad layout to the
-    // MFMA layout (same node and channel group, different lane)
+    // a_i x~_i and the value accumulators move to the MFMA layout:
+    //   X~^T B operand, k block kb: lane (l16, mlg) holds channels 32 kb + 8 mlg + e
+    //   O^T accumulator, tile n:    lane (l16, mlg) holds channels 16 n + 4 mlg + e
+    float xm[KB][8];
 #pragma unroll
-    for (int c = 0; c < KPL; ++c) x[c] = lane_gather(x[c] * r, src_lane);
+    for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
-    for (int c = 0; c < 4 * NT; ++c) acc[c] = lane_gather(acc[c], src_lane);
+      for (int e = 0; e < 8; ++e) {
+        int rr, src;
+        bool valid = true;
+        if constexpr (DK >= 32) {
+          rr = 4 * kb + (e & 3);
+          src = sbase + 2 * mlg + (e >> 2);
+        } else {
+          rr = e & 1;
+          src = (sbase + 4 * mlg + (e >> 1)) & 63;
+          valid = mlg < 2;
+        }
+        const float a0 = lane_gather(x[0][rr], src);
+        const float a1 = lane_gather(x[1][rr], src);
+        xm[kb][e] = valid ? (mhalf ? a1 : a0) : 0.0f;
+        pin(xm[kb][e]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    float am[NT][4];
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        int rr, src;
+        if constexpr (DVS >= 32) {
+          rr = 4 * (n >> 1) + e;
+          src = sbase + 4 * (n & 1) + mlg;
+        } else {
+          rr = e & 1;
+          src = sbase + 2 * mlg + (e >> 1);
+        }
+        const float a0 = lane_gather(acc[0][rr], src);
+        const float a1 = lane_gather(acc[1][rr], src);
+        am[n][e] = mhalf ? a1 : a0;
+        pin(am[n][e]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     __syncthreads();  // v~ consumed
 
-    // 2d: S0 of this head -> LDS as bf16 hi/lo planes [DVS][KAPPA + kSPad].
-    //     The MFMA k index kappa = 32 kb + 8 lg + 4 h + e holds key channel
-    //     32 kb + 16 h + 4 lg + e, the channel that MFMA lane group lg holds
-    //     in register 8 kb + 4 h + e of the pulled-back query.
+    // 2d: S0 of this head -> LDS as bf16 hi/lo planes [DVS][KAPPA + kSPad]
+    //     (key channels in natural order, 16..31 zero for dk = 16)
     {
       uint16_t* s_hi = reinterpret_cast<uint16_t*>(s_rv);
       uint16_t* s_lo = s_hi + DVS * (KAPPA + kSPad);
@@ -490,55 +634,54 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       for (int j = 0; j < NS0; ++j) {
         const int idx = j * kVT + tid;
         if (NS0 * kVT == DVS * DK / 4 || idx < DVS * DK / 4) {
-          const int row = idx / (DK / 4), mch = idx % (DK / 4);  // physical chunk m
-          const int kch = 8 * (mch / 8) + 2 * (mch % 4) + (mch / 4) % 2;
-          uint2 hi, lo;
-          split4(s0pf[j], hi, lo);
+          const int row = idx / (DK / 4), kch = idx % (DK / 4);
+          uint2 hi, lo2;
+          split4(s0pf[j], hi, lo2);
           *reinterpret_cast<uint2*>(s_hi + row * (KAPPA + kSPad) + 4 * kch) = hi;
-          *reinterpret_cast<uint2*>(s_lo + row * (KAPPA + kSPad) + 4 * kch) = lo;
+          *reinterpret_cast<uint2*>(s_lo + row * (KAPPA + kSPad) + 4 * kch) = lo2;
         }
       }
-      if (DK < 32) {  // odd kappa chunks carry no channel: zero them
+      if (DK < 32) {
         for (int i = tid; i < DVS * 4; i += kVT) {
-          const int row = i / 4, kch = 2 * (i % 4) + 1;
+          const int row = i / 4, kch = 4 + i % 4;
           *reinterpret_cast<uint2*>(s_hi + row * (KAPPA + kSPad) + 4 * kch) = make_uint2(0, 0);
           *reinterpret_cast<uint2*>(s_lo + row * (KAPPA + kSPad) + 4 * kch) = make_uint2(0, 0);
         }
       }
     }
-    if (hh + 1 < p.hpw)
+    __builtin_amdgcn_sched_barrier(0);  // this head's S0 registers are free before the next loads
+    // the next head's raw values, gates and S0 load during the MFMA phase;
+    // S0 is issued last, so the wait for the others in the next 2a leaves
+    // it in flight
+    if (hh + 1 < p.hpw) {
+      prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
+      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
       prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, tid, s0pf);
+    }
     __syncthreads();
 
     // 2e: O^T = S0 X~^T + ACC^T on MFMA (MFMA layout); store
-    if (wave * 16 < TP) {
+    {
       bf16x8 xh[KB], xl[KB];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        float x8[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x8[e] = (8 * kb + e < KPL) ? x[(8 * kb + e) % KPL] : 0.0f;
-        split8(x8, xh[kb], xl[kb]);
-      }
+      for (int kb = 0; kb < KB; ++kb) split8(xm[kb], xh[kb], xl[kb]);
       const uint16_t* s_hi = reinterpret_cast<const uint16_t*>(s_rv);
       const uint16_t* s_lo = s_hi + DVS * (KAPPA + kSPad);
       const int node = mpos < T ? s_ord[mpos] : 0;
       float* orow_p = p.out + (size_t(b) * T + node) * orow + size_t(h) * DV + c0;
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        {
-          f32x4 d = {acc[4 * n], acc[4 * n + 1], acc[4 * n + 2], acc[4 * n + 3]};
+        f32x4 d = {am[n][0], am[n][1], am[n][2], am[n][3]};
 #pragma unroll
-          for (int kb = 0; kb < KB; ++kb) {
-            const int off = (16 * n + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg;
-            const bf16x8 ah = *reinterpret_cast<const bf16x8*>(s_hi + off);
-            const bf16x8 al = *reinterpret_cast<const bf16x8*>(s_lo + off);
-            d = mfma3(ah, al, xh[kb], xl[kb], d);
-          }
-          if (mpos < T)
-            *reinterpret_cast<float4*>(orow_p + 16 * n + 4 * mlg) =
-                make_float4(d[0] * p.scale, d[1] * p.scale, d[2] * p.scale, d[3] * p.scale);
+        for (int kb = 0; kb < KB; ++kb) {
+          const int off = (16 * n + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg;
+          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(s_hi + off);
+          const bf16x8 al = *reinterpret_cast<const bf16x8*>(s_lo + off);
+          d = mfma3(ah, al, xh[kb], xl[kb], d);
         }
+        if (mpos < T)
+          *reinterpret_cast<float4*>(orow_p + 16 * n + 4 * mlg) =
+              make_float4(d[0] * p.scale, d[1] * p.scale, d[2] * p.scale, d[3] * p.scale);
       }
     }
     __syncthreads();  // S0 planes consumed before the next head reuses the region
