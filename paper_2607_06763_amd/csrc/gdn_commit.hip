@@ -2,11 +2,11 @@
 // accepted leaf is known a single pass replays Eq. 7 along its path and
 // writes the state; it is the only state write of the decode step).
 //
-// Kernel 1 (grid Hv x B, 512 threads): the state loads are issued first; the
-// path root..a of the accepted slot a is read off its ancestor bitmask; each
-// half of the workgroup featurises half of a chunk of kChunk path nodes (one
-// thread per feature channel, width-4 conv window along the path, conv-state
-// slots above the root) into LDS, with the key norms reduced across waves;
+// Kernel 1 (grid Hv x B, 512 threads): the path root..a of the accepted slot
+// a is read off its ancestor bitmask; one thread per (feature channel, half
+// of a chunk of 32 path nodes) slides the width-4 conv window along the path
+// (conv-state slots above the root) into LDS, its raw inputs loaded before
+// the state rows; the key norms are reduced per path node;
 // each row of S[b][h] (dv rows of dk) lives in the registers of LPR lanes and
 // takes one rank-1 step per path node,
 //     S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T,
@@ -22,8 +22,10 @@ namespace gdn {
 
 // threads per state workgroup: 512, or one per state element for tiny heads
 constexpr int commit_threads(int dk, int dv) { return dk * dv >= 512 ? 512 : dk * dv; }
-constexpr int kChunk = 16;   // path nodes featurised per LDS chunk
-constexpr int kCMaxT = 128;  // tree slots supported
+constexpr int kCMaxT = 128;    // tree slots supported
+constexpr int kMC = 32;        // path nodes featurised per chunk
+constexpr int kMH = kMC / 2;   // path nodes per feature half
+constexpr int kWin = kMH + 3;  // raw conv window of one half
 
 struct CommitParams {
   int B, T, Hk, Hv;
@@ -46,58 +48,114 @@ __device__ __forceinline__ int commit_check(const MetaPtrs& m, int b, int T, int
   return GDN_TREE_OK;
 }
 
+// Inputs of one feature task (a channel over one half of a path chunk).
+// Every load is unconditional (indices clamped) so that nothing waits for
+// it before the features are computed; the conv-state / padding choice is
+// made when the window is used.
+template <typename TIn>
+struct FeatWindow {
+  TIn xr[kWin];  // raw inputs of path nodes m0 - 3 .. m0 + kMH - 1 (clamped)
+  float xc[3];   // conv-state slots 0..2 of the channel
+  float4 w;      // conv weights of the channel
+  __device__ __forceinline__ void load(const TIn* src, size_t stride, const float* cs, size_t cstride,
+                                       const float* wrow, const int* s_path, int m0, int L) {
+#pragma unroll
+    for (int q = 0; q < kWin; ++q) {
+      int mi = m0 - 3 + q;
+      mi = mi < 0 ? 0 : (mi < L ? mi : L - 1);
+      xr[q] = src[size_t(s_path[mi]) * stride];
+    }
+#pragma unroll
+    for (int sl = 0; sl < 3; ++sl) xc[sl] = cs[size_t(sl) * cstride];
+    w = *reinterpret_cast<const float4*>(wrow);
+  }
+  // input of the window element q (path node m0 - 3 + q); the conv-state
+  // slot is picked by selects, not by indexing (keeps xc in registers)
+  __device__ __forceinline__ float x(int q, int m0, int L) const {
+    const int mi = m0 - 3 + q;
+    const float c = mi == -3 ? xc[0] : (mi == -2 ? xc[1] : xc[2]);
+    return mi < 0 ? c : (mi < L ? to_f32(xr[q]) : 0.0f);
+  }
+};
+
 template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(CommitParams p) {
   constexpr int kCT = commit_threads(DK, DV);
   constexpr int EPT = DV * DK / kCT;  // state elements per thread
   constexpr int LPR = DK / EPT;       // lanes per state row (power of 2)
-  constexpr int NCH = DK + DV;        // feature channels: k of key head g, v of head h
-  constexpr int HALF = kCT / 2;       // threads per feature half
-  constexpr int CPT = (NCH + HALF - 1) / HALF;  // feature channels per thread
-  constexpr int MH = kChunk / 2;      // path nodes per half and chunk
   static_assert(EPT >= 1 && (EPT < 4 || EPT % 4 == 0), "state split");
   static_assert(LPR >= 1 && LPR <= 32 && (LPR & (LPR - 1)) == 0, "row lanes");
+  static_assert(2 * (DK + DV) <= kCT, "one feature task per thread");
 
   __shared__ int s_path[kCMaxT];
   __shared__ int s_dep[kCMaxT];
-  __shared__ float s_al[kCMaxT], s_be[kCMaxT];
-  __shared__ __align__(16) float s_f[kChunk][NCH];  // conv+SiLU features of a path chunk
-  __shared__ float s_part[kChunk][kCT / kWave];     // per-wave partial sums of k^2
-  __shared__ float s_inv[kChunk];                   // 1 / ||k|| per path node
+  __shared__ float s_al[kCMaxT], s_be[kCMaxT];    // gates by path index
+  __shared__ __align__(16) float s_fk[kMC][DK];  // SiLU(conv) keys of a path chunk (unnormalised)
+  __shared__ __align__(16) float s_fv[kMC][DV];  // SiLU(conv) values of a path chunk
+  __shared__ float s_inv[kMC];                    // 1 / ||k|| per path node of the chunk
 
   const int h = blockIdx.x, b = blockIdx.y;
   const int T = p.T, Hk = p.Hk, Hv = p.Hv;
   const int g = h * Hk / Hv;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x;
   const int C = 2 * Hk * DK + Hv * DV;
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
   const TIn* alpha = static_cast<const TIn*>(p.alpha);
   const TIn* beta = static_cast<const TIn*>(p.beta);
 
-  // first round of loads: nothing here depends on the accepted slot
+  // ---- first round: statuses, depths and gates of all slots (raw gates are
+  //      converted only once the path is known)
   const int a = p.accepted[b];
   const int tree_st = m.status[b];
-  int dep_j = -1;
-  float al_j = 0.0f, be_j = 0.0f;
-  if (tid < T) {
-    dep_j = m.depth[size_t(b) * T + tid];
-    const size_t ab = (size_t(b) * T + tid) * Hv + h;
-    al_j = ld(alpha, ab);
-    be_j = ld(beta, ab);
-  }
+  const int tj = tid < T ? tid : T - 1;
+  const int dep_j = m.depth[size_t(b) * T + tj];
+  const TIn al_j = alpha[(size_t(b) * T + tj) * Hv + h];
+  const TIn be_j = beta[(size_t(b) * T + tj) * Hv + h];
   if (tree_st != GDN_TREE_OK || a < 0 || a >= T) {
     if (h == 0 && tid == 0 && p.commit_status)
       p.commit_status[b] = tree_st != GDN_TREE_OK ? tree_st : (a == -1 ? GDN_TREE_OK : GDN_TREE_BAD_ACCEPTED);
     return;
   }
+  // ---- second round: the ancestor bitmask of a -> the path root..a
+  const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (tj >> 6)];
+  if (tid < T) s_dep[tid] = dep_j;
+  __syncthreads();
+  const int d = s_dep[a];
+  if (h == 0 && tid == 0 && p.commit_status)
+    p.commit_status[b] = d < 0 ? GDN_TREE_BAD_ACCEPTED : GDN_TREE_OK;
+  if (d < 0) return;  // accepted slot is padding
+  if (tid < T && (tid == a || ((word >> (tid & 63)) & 1ull))) {
+    s_path[dep_j] = tid;
+    s_al[dep_j] = to_f32(al_j);
+    s_be[dep_j] = to_f32(be_j);
+  }
+  __syncthreads();
+  const int L = d + 1;  // path length
+
+  // ---- feature task of this thread: value channel (tid < 2 DV) or key
+  //      channel (2 DV <= tid < 2 (DV + DK)); fhalf picks the half of a chunk
+  const bool vtask = tid < 2 * DV;
+  const bool ktask = !vtask && tid < 2 * (DV + DK);
+  const int tt = vtask ? tid : tid - 2 * DV;
+  const int fc = vtask ? tt % DV : tt % DK;
+  const int fhalf = vtask ? tt / DV : tt / DK;
+  const int fch = vtask ? 2 * Hk * DK + h * DV + fc : Hk * DK + g * DK + fc;  // conv channel
+  const TIn* fsrc = vtask ? static_cast<const TIn*>(p.v) + size_t(b) * T * Hv * DV + size_t(h) * DV + fc
+                          : static_cast<const TIn*>(p.k) + size_t(b) * T * Hk * DK + size_t(g) * DK + fc;
+  const size_t fstride = vtask ? size_t(Hv) * DV : size_t(Hk) * DK;
+  const float* fcs = p.conv_state + size_t(b) * 3 * C + fch;
+  FeatWindow<TIn> win;
+  if (vtask || ktask) win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_path, fhalf * kMH, L);
+
+  // ---- the state rows load behind the first windows
   const int row = tid / LPR;
   const int col0 = (tid % LPR) * EPT;
-  float* Sbh = p.S + (size_t(b) * Hv + h) * size_t(DV) * DK;
-  float srow[EPT];  // state rows in registers; the loads overlap the path work
+  float* Sbh = p.S + (size_t(b) * Hv + h) * size_t(DV) * DK + size_t(row) * DK + col0;
+  float srow[EPT];
   if constexpr (EPT % 4 == 0) {
 #pragma unroll
     for (int e = 0; e < EPT; e += 4) {
-      const float4 x = *reinterpret_cast<const float4*>(Sbh + size_t(row) * DK + col0 + e);
+      const float4 x = *reinterpret_cast<const float4*>(Sbh + e);
       srow[e] = x.x;
       srow[e + 1] = x.y;
       srow[e + 2] = x.z;
@@ -105,94 +163,47 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
     }
   } else {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) srow[e] = Sbh[size_t(row) * DK + col0 + e];
+    for (int e = 0; e < EPT; ++e) srow[e] = Sbh[e];
   }
-  if (tid < T) s_dep[tid] = dep_j;
-  __syncthreads();
-  const int d = s_dep[a];
-  if (h == 0 && tid == 0 && p.commit_status)
-    p.commit_status[b] = d < 0 ? GDN_TREE_BAD_ACCEPTED : GDN_TREE_OK;
-  if (d < 0) return;  // accepted slot is padding
-
-  // second round: the path root..a from the ancestor bitmask of a
-  if (tid < T) {
-    const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (tid >> 6)];
-    if (tid == a || ((word >> (tid & 63)) & 1ull)) {
-      s_path[dep_j] = tid;
-      s_al[dep_j] = al_j;
-      s_be[dep_j] = be_j;
-    }
-  }
-
-  // feature channels of this thread: c < DK -> k[g][c], else v[h][c - DK]
-  const int half = tid / HALF, ht = tid % HALF;
-  const TIn* kin = static_cast<const TIn*>(p.k);
-  const TIn* vin = static_cast<const TIn*>(p.v);
-  const size_t krow = size_t(Hk) * DK, vrow = size_t(Hv) * DV;
-  float wt[CPT][4];
-  const TIn* src[CPT];
-  size_t sstride[CPT];
-  const float* csrc[CPT];
-#pragma unroll
-  for (int u = 0; u < CPT; ++u) {
-    const int c = ht + u * HALF;
-    const int cc = c < NCH ? c : 0;
-    const int ch = cc < DK ? Hk * DK + g * DK + cc : 2 * Hk * DK + h * DV + (cc - DK);
-    src[u] = cc < DK ? kin + size_t(b) * T * krow + size_t(g) * DK + cc
-                     : vin + size_t(b) * T * vrow + size_t(h) * DV + (cc - DK);
-    sstride[u] = cc < DK ? krow : vrow;
-    csrc[u] = p.conv_state + size_t(b) * 3 * C + ch;
-    const float4 w4 = *reinterpret_cast<const float4*>(p.conv_w + size_t(ch) * 4);
-    wt[u][0] = w4.x;
-    wt[u][1] = w4.y;
-    wt[u][2] = w4.z;
-    wt[u][3] = w4.w;
-  }
-  __syncthreads();  // s_path ready
 
   // S_true = gamma * srow: one step costs one FMA for S.k and one for the
   // rank-1 write, S_true <- alpha S_true + c k  <=>  srow += c / (alpha gamma) k
   float gamma = 1.0f;
-  for (int base = 0; base <= d; base += kChunk) {
-    const int cnt = (d - base + 1) < kChunk ? (d - base + 1) : kChunk;
-    // this half featurises path nodes base + half * MH .. + MH - 1; the
-    // window before its first node comes from the path or the conv state
-    const int m0 = base + half * MH;
-    float ksq[MH];
+  for (int base = 0; base < L; base += kMC) {
+    if (base > 0 && (vtask || ktask))  // long paths: later chunks load here
+      win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_path, base + fhalf * kMH, L);
+    // features of the chunk (window element q is path node m0 - 3 + q)
+    if (vtask || ktask) {
+      const int m0 = base + fhalf * kMH;
 #pragma unroll
-    for (int mr = 0; mr < MH; ++mr) ksq[mr] = 0.0f;
-#pragma unroll
-    for (int u = 0; u < CPT; ++u) {
-      const int c = ht + u * HALF;
-      float xs[MH + 3];
-#pragma unroll
-      for (int q = 0; q < MH + 3; ++q) {
-        const int mi = m0 - 3 + q;  // path index of this window element
-        xs[q] = mi < 0 ? csrc[u][size_t(3 + mi) * C]
-                       : (mi <= d ? ld(src[u], size_t(s_path[mi]) * sstride[u]) : 0.0f);
-      }
-#pragma unroll
-      for (int mr = 0; mr < MH; ++mr) {
-        const float y = silu(wt[u][0] * xs[mr] + wt[u][1] * xs[mr + 1] + wt[u][2] * xs[mr + 2] +
-                             wt[u][3] * xs[mr + 3]);
-        if (c < NCH) s_f[half * MH + mr][c] = y;
-        if (c < DK) ksq[mr] += y * y;
+      for (int mr = 0; mr < kMH; ++mr) {
+        const float y = silu(win.w.x * win.x(mr, m0, L) + win.w.y * win.x(mr + 1, m0, L) +
+                             win.w.z * win.x(mr + 2, m0, L) + win.w.w * win.x(mr + 3, m0, L));
+        if (vtask)
+          s_fv[fhalf * kMH + mr][fc] = y;
+        else
+          s_fk[fhalf * kMH + mr][fc] = y;
       }
     }
-    // ||k||^2 per path node: wave sums, then across the waves of the half
+    __syncthreads();
+    // key norms: 16 lanes per path node, DK / 16 channels per lane
 #pragma unroll
-    for (int mr = 0; mr < MH; ++mr) {
-      const float v = wave_sum(ksq[mr]);
-      if (lane == 0) s_part[half * MH + mr][wave % (HALF / kWave)] = v;
+    for (int nd0 = 0; nd0 < kMC; nd0 += kCT / 16) {
+      constexpr int CPL = DK / 16;
+      const int nd = nd0 + (tid >> 4), ln = tid & 15;
+      float ss = 0.0f;
+      if (nd < kMC) {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          const float y = s_fk[nd][ln * CPL + c];
+          ss += y * y;
+        }
+      }
+      ss = group_sum<16>(ss);
+      if (nd < kMC && ln == 0) s_inv[nd] = rsqrt_hw(ss + 1e-6f);
     }
     __syncthreads();
-    if (tid < kChunk) {
-      float v = 0.0f;
-#pragma unroll
-      for (int wv = 0; wv < HALF / kWave; ++wv) v += s_part[tid][wv];
-      s_inv[tid] = rsqrt_hw(v + 1e-6f);
-    }
-    __syncthreads();
+    const int cnt = L - base < kMC ? L - base : kMC;
     for (int mr = 0; mr < cnt; ++mr) {
       const int mi = base + mr;
       const float al = s_al[mi], be = s_be[mi], inv = s_inv[mr];
@@ -200,7 +211,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
       if constexpr (EPT % 4 == 0) {
 #pragma unroll
         for (int e = 0; e < EPT; e += 4) {
-          const float4 x = *reinterpret_cast<const float4*>(&s_f[mr][col0 + e]);
+          const float4 x = *reinterpret_cast<const float4*>(&s_fk[mr][col0 + e]);
           kk[e] = x.x;
           kk[e + 1] = x.y;
           kk[e + 2] = x.z;
@@ -208,7 +219,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) kk[e] = s_f[mr][col0 + e];
+        for (int e = 0; e < EPT; ++e) kk[e] = s_fk[mr][col0 + e];
       }
       float u0 = 0.0f, u1 = 0.0f;
 #pragma unroll
@@ -221,7 +232,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
       // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
       // multiplied by 1 / ||k|| so that it applies to the raw key
       const float ag = al * gamma;
-      const float c = be * (s_f[mr][DK + row] - ag * uu) * __builtin_amdgcn_rcpf(ag) * inv;
+      const float c = be * (s_fv[mr][row] - ag * uu) * __builtin_amdgcn_rcpf(ag) * inv;
 #pragma unroll
       for (int e = 0; e < EPT; ++e) srow[e] += c * kk[e];
       gamma = ag;
@@ -236,11 +247,11 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
   if constexpr (EPT % 4 == 0) {
 #pragma unroll
     for (int e = 0; e < EPT; e += 4)
-      *reinterpret_cast<float4*>(Sbh + size_t(row) * DK + col0 + e) =
+      *reinterpret_cast<float4*>(Sbh + e) =
           make_float4(srow[e] * gamma, srow[e + 1] * gamma, srow[e + 2] * gamma, srow[e + 3] * gamma);
   } else {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) Sbh[size_t(row) * DK + col0 + e] = srow[e] * gamma;
+    for (int e = 0; e < EPT; ++e) Sbh[e] = srow[e] * gamma;
   }
 }
 

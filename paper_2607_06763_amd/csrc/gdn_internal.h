@@ -122,17 +122,18 @@ constexpr int kDppQuadXor2 = 0x4E;      // quad_perm [2,3,0,1]
 constexpr int kDppRowHalfMirror = 0x141;  // lane i <-> 7-i within each 8 lanes
 constexpr int kDppRowMirror = 0x140;      // lane i <-> 15-i within each 16 lanes
 
-// Sum over aligned groups of N consecutive lanes (N = 1, 2, ..., 32); every
+// Sum over aligned groups of N consecutive lanes (N = 1, 2, ..., 64); every
 // lane of a group receives the group's sum.  Up to 16 lanes this is DPP only;
-// the step across 16-lane rows goes through ds_bpermute.
+// the steps across 16-lane rows go through ds_bpermute.
 template <int N>
 __device__ __forceinline__ float group_sum(float v) {
-  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16 || N == 32, "group size");
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8 || N == 16 || N == 32 || N == 64, "group size");
   if constexpr (N >= 2) v += dpp_f<kDppQuadXor1>(v);
   if constexpr (N >= 4) v += dpp_f<kDppQuadXor2>(v);
   if constexpr (N >= 8) v += dpp_f<kDppRowHalfMirror>(v);
   if constexpr (N >= 16) v += dpp_f<kDppRowMirror>(v);
   if constexpr (N >= 32) v += __shfl_xor(v, 16);
+  if constexpr (N >= 64) v += __shfl_xor(v, 32);
   return v;
 }
 
@@ -142,6 +143,40 @@ __device__ __forceinline__ float wave_sum(float v) {
   const int b = __float_as_int(v);
   return __int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16)) +
          __int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48));
+}
+
+// ---------------------------------------------------------------------------
+// MFMA helpers: v_mfma_f32_16x16x32_bf16 operands and a bf16 hi/lo split
+// that keeps about 16 bits of the fp32 mantissa (three products per tile).
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 hi/lo split by truncation: x = hi + lo + O(2^-16 |x|).
+__device__ __forceinline__ void split8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
+  u32x4 h, l;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    uint32_t u0 = __float_as_uint(x[2 * e]), u1 = __float_as_uint(x[2 * e + 1]);
+    uint32_t h0 = u0 & 0xffff0000u, h1 = u1 & 0xffff0000u;
+    float r0 = x[2 * e] - __uint_as_float(h0);
+    float r1 = x[2 * e + 1] - __uint_as_float(h1);
+    h[e] = (h0 >> 16) | h1;
+    l[e] = (__float_as_uint(r0) >> 16) | (__float_as_uint(r1) & 0xffff0000u);
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+// Three bf16 products of a hi/lo split pair into an fp32 accumulator:
+// (ah + al)(bh + bl) - al bl, ~1e-5 relative error.
+__device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const bf16x8& bh,
+                                       const bf16x8& bl, f32x4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, c, 0, 0, 0);
+  return c;
 }
 
 // ---------------------------------------------------------------------------

@@ -47,9 +47,6 @@
 
 namespace gdn {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kVT = 512;        // threads per workgroup (8 waves)
 constexpr int kVMaxT = 128;     // tree slots supported = 8 waves x 16 nodes
@@ -131,22 +128,6 @@ __device__ __forceinline__ int row_off(int t) {
   return (t << __builtin_ctz(D)) + (t << 2);
 }
 
-// bf16 hi/lo split by truncation: x = hi + lo + O(2^-16 |x|).
-__device__ __forceinline__ void split8(const float (&x)[8], bf16x8& hi, bf16x8& lo) {
-  u32x4 h, l;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    uint32_t u0 = __float_as_uint(x[2 * e]), u1 = __float_as_uint(x[2 * e + 1]);
-    uint32_t h0 = u0 & 0xffff0000u, h1 = u1 & 0xffff0000u;
-    float r0 = x[2 * e] - __uint_as_float(h0);
-    float r1 = x[2 * e + 1] - __uint_as_float(h1);
-    h[e] = (h0 >> 16) | h1;
-    l[e] = (__float_as_uint(r0) >> 16) | (__float_as_uint(r1) & 0xffff0000u);
-  }
-  hi = __builtin_bit_cast(bf16x8, h);
-  lo = __builtin_bit_cast(bf16x8, l);
-}
-
 // 4 floats -> packed bf16 hi (2 dwords) and lo (2 dwords), truncation split
 __device__ __forceinline__ void split4(float4 x, uint2& hi, uint2& lo) {
   const float xs[4] = {x.x, x.y, x.z, x.w};
@@ -159,14 +140,6 @@ __device__ __forceinline__ void split4(float4 x, uint2& hi, uint2& lo) {
   }
   hi = make_uint2((h[0] >> 16) | h[1], (h[2] >> 16) | h[3]);
   lo = make_uint2((l[0] >> 16) | l[1], (l[2] >> 16) | l[3]);
-}
-
-__device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const bf16x8& bh,
-                                       const bf16x8& bl, f32x4 c) {
-  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, c, 0, 0, 0);
-  return c;
 }
 
 // Pins x to a register at this point: keeps the compiler from sinking the
