@@ -4,6 +4,10 @@
 One step = one pass of the whole hot path for one GDN layer over one batch of
 synthetic draft trees: tree prepare, verify (every node's output from the
 read-only cached state) and commit (state + conv state of the accepted node).
+By default a step is timed as a decode loop runs it: prepare of the current
+tree, then one fused launch that commits the previous step's accepted node
+and verifies the current tree against the state it produces (--unfused: three
+separate launches, prepare / verify / commit).
 The default workload is the large one: 32 trees of 128 nodes (depth 16),
 16 key / 48 value heads, dk = dv = 128, bf16 inputs, fp32 state.
 
@@ -63,12 +67,15 @@ def algorithmic_bytes(w) -> dict:
     commit = (2 * 4 * B * Hv * dv * dk + 2 * 4 * 3 * B * C + int(L) * (e * C + 2 * e * Hv)
               + 4 * 4 * C + 8 * B * T + 8 * B)
     prepare = 4 * B * T + 8 * B * T * ((T + 63) // 64) + 4 * 4 * B * T + 8 * B
-    return {"verify": int(verify), "commit": int(commit), "prepare": int(prepare)}
+    # fused step: S, the conv state and the conv weights are read once
+    fused = verify + commit - 4 * B * Hv * dv * dk - 4 * 3 * B * C - 4 * 4 * C
+    return {"verify": int(verify), "commit": int(commit), "prepare": int(prepare),
+            "step": int(fused)}
 
 
-def measured_traffic(src_hash: str):
-    """HBM bytes per verify launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source; else None."""
+def measured_traffic(src_hash: str, kernel: str):
+    """HBM bytes per launch of kernel from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     vals = {}
@@ -77,7 +84,7 @@ def measured_traffic(src_hash: str):
             if ":" in line and line.startswith("- "):
                 k, v = line[2:].split(":", 1)
                 vals[k.strip()] = v.strip().strip("`")
-    if vals.get("verify_source_sha256_16") != src_hash:
+    if vals.get("verify_source_sha256_16") != src_hash or vals.get("kernel", "verify") != kernel:
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -125,6 +132,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4, help="workload index 0..4 (default: large)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time prepare, verify and commit as three launches (default: prepare + "
+                         "the fused commit-then-verify step)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="after timing, run 5 plain device copies of this many MiB (a known-size "
                          "kernel for scaling HBM counters)")
@@ -153,9 +163,32 @@ def main() -> int:
     cs = dt.conv_state.clone()
     nbytes = algorithmic_bytes(w)
 
-    def step(ev=None):
+    nodes = w.B * w.T
+    fused = not args.unfused
+    # two metadata buffers and two conv-state buffers alternate between steps:
+    # the fused launch reads the previous tree's metadata and conv state while
+    # the current tree's are written
+    metas = [dt.meta, torch.zeros_like(dt.meta)]
+    css = [cs, torch.empty_like(cs)]
+    # the previous step's raw inputs live in their own buffers (same values):
+    # the commit reads them from HBM, not from what the verify just cached
+    prev = {n: getattr(dt, n).clone() for n in ("q", "k", "v", "alpha", "beta")} if fused else {}
+    nev = 3 if fused else 4
+
+    def step(i, ev=None):
         if ev is not None:
             ev[0].record()
+        if fused:
+            cur, pmeta = metas[i % 2], metas[(i + 1) % 2]
+            G.prepare(dt.dims, dt.parent, cur, dt.tree_status)
+            if ev is not None:
+                ev[1].record()
+            G.step(dt.dims, pmeta, dt.accepted, prev["q"], prev["k"], prev["v"], prev["alpha"],
+                   prev["beta"], dt.commit_status, cur, dt.q, dt.k, dt.v, dt.alpha, dt.beta,
+                   dt.conv_w, css[i % 2], css[(i + 1) % 2], S, dt.out)
+            if ev is not None:
+                ev[2].record()
+            return
         dt.prepare()
         if ev is not None:
             ev[1].record()
@@ -166,30 +199,54 @@ def main() -> int:
         if ev is not None:
             ev[3].record()
 
-    for _ in range(args.warmup):
-        step()
+    if fused:
+        G.prepare(dt.dims, dt.parent, metas[1], dt.tree_status)  # the "previous" tree of step 0
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(events[i])
+        step(args.warmup + i, events[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
-                    for e in events]) * 1e3  # us
-    us_prep, us_ver, us_com = (float(x) for x in per.mean(0))
-    p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
-
-    nodes = w.B * w.T
-    ach = nbytes["verify"] / (us_ver * 1e-6) / 1e9
+    per = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(nev - 1)] for e in events]) * 1e3
     src_hash = verify_source_hash()
-    traffic = measured_traffic(src_hash)
+    if fused:
+        us_prep, us_main = (float(x) for x in per.mean(0))
+        kname, kbytes = "step", nbytes["step"]
+    else:
+        us_prep, us_main, us_com = (float(x) for x in per.mean(0))
+        kname, kbytes = "verify", nbytes["verify"]
+    p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
+    ach = kbytes / (us_main * 1e-6) / 1e9
+    traffic = measured_traffic(src_hash, kname)
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "verify", "algorithmic_bytes_per_launch": nbytes["verify"],
-                "avg_launch_us": round(us_ver, 3)}
+                "kernel": kname, "algorithmic_bytes_per_launch": kbytes,
+                "avg_launch_us": round(us_main, 3)}
+    if fused:
+        detail = {
+            "us_prepare": round(us_prep, 3), "us_step": round(us_main, 3),
+            "us_step_p10_p50_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
+            "step_hbm_frac": round(ach / HBM_PEAK_GBS, 4),
+        }
+    else:
+        detail = {
+            "us_prepare": round(us_prep, 3), "us_verify": round(us_main, 3),
+            "us_verify_p10_p50_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
+            "us_commit": round(us_com, 3),
+            "nodes_per_s_verify_only": round(nodes / (us_main * 1e-6), 1),
+            "verify_hbm_frac": round(ach / HBM_PEAK_GBS, 4),
+            "commit_GBs": round(nbytes["commit"] / (us_com * 1e-6) / 1e9, 1),
+            "verify_plus_commit_hbm_frac": round(
+                (nbytes["verify"] + nbytes["commit"]) / ((us_main + us_com) * 1e-6) / 1e9
+                / HBM_PEAK_GBS, 4),
+        }
+    detail["algorithmic_bytes"] = nbytes
+    detail["verify_source_sha256_16"] = src_hash
     out = {
         "metric": "tree nodes verified/s per GDN layer",
         "value": round(nodes / (ms_step * 1e-3), 1),
@@ -205,21 +262,11 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": f"{w.name}: B={w.B} trees x T={w.T} nodes, Hk={w.Hk} Hv={w.Hv} "
                                f"dk={w.dk} dv={w.dv}, {w.in_dtype} inputs, fp32 state and output",
-                   "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)"},
+                   "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)",
+                   "step": "prepare + fused commit/verify" if fused else
+                           "prepare + verify + commit"},
         "roofline": roofline,
-        "detail": {
-            "us_prepare": round(us_prep, 3), "us_verify": round(us_ver, 3),
-            "us_verify_p10_p50_p90": [round(p10, 3), round(p50, 3), round(p90, 3)],
-            "us_commit": round(us_com, 3),
-            "nodes_per_s_verify_only": round(nodes / (us_ver * 1e-6), 1),
-            "verify_hbm_frac": round(ach / HBM_PEAK_GBS, 4),
-            "commit_GBs": round(nbytes["commit"] / (us_com * 1e-6) / 1e9, 1),
-            "verify_plus_commit_hbm_frac": round(
-                (nbytes["verify"] + nbytes["commit"]) / ((us_ver + us_com) * 1e-6) / 1e9
-                / HBM_PEAK_GBS, 4),
-            "algorithmic_bytes": nbytes,
-            "verify_source_sha256_16": src_hash,
-        },
+        "detail": detail,
     }
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib * (1 << 20) // 4

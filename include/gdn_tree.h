@@ -150,6 +150,39 @@ int gdn_tree_commit(const gdn_dims* dims, const void* meta, const int32_t* accep
                     const void* beta, const float* conv_w, float* conv_state, float* S,
                     int32_t* commit_status, hipStream_t stream);
 
+/* Fused decode step: the commit of the previous step's accepted node
+ * (Sec. 3.4.2) followed by the verification of the current tree (Sec. 3.4,
+ * Eq. 7-8) against the state it produces, in one launch.  Results equal
+ * gdn_tree_commit(previous step) followed by gdn_tree_verify(current step)
+ * with the committed S and conv state; the committed state is formed in
+ * registers and verified against without being read back.
+ *   prev_meta      meta of the previous step's tree (same B, T)
+ *   prev_accepted  int32 [B]: accepted slot of the previous tree, -1 = none
+ *   prev_q, prev_k, prev_v, prev_alpha, prev_beta: the previous step's raw
+ *                  inputs (shapes and in_dtype as for verify)
+ *   commit_status  int32 [B] (may be NULL): as for gdn_tree_commit
+ *   meta, q, k, v, alpha, beta: the current step's tree and raw inputs
+ *   conv_w         fp32 [C][4] (one layer: shared by both steps)
+ *   conv_state     fp32 [B][3][C]  read-only: conv state before the commit
+ *   conv_state_out fp32 [B][3][C]  written: conv state after the commit; must
+ *                  not overlap conv_state (checked, GDN_EINVAL)
+ *   S              fp32 [B][Hv][dv][dk]  in/out: the state before the commit
+ *                  on entry, after it on return
+ *   out            fp32 [B][T][Hv][dv]  written: outputs of the current tree
+ * A sequence with nothing to commit (prev_accepted -1 or a non-zero commit
+ * status) keeps S and gets conv_state_out = conv_state; a sequence whose
+ * current tree is invalid still commits and gets zero outputs.  Each
+ * (sequence, value head, dv slice) of S is read and written by one
+ * workgroup only, so the in-place update is race-free; S must not alias
+ * any other argument. */
+int gdn_tree_step(const gdn_dims* dims, const void* prev_meta, const int32_t* prev_accepted,
+                  const void* prev_q, const void* prev_k, const void* prev_v,
+                  const void* prev_alpha, const void* prev_beta, int32_t* commit_status,
+                  const void* meta, const void* q, const void* k, const void* v,
+                  const void* alpha, const void* beta, const float* conv_w,
+                  const float* conv_state, float* conv_state_out, float* S, float* out,
+                  hipStream_t stream);
+
 /* Message describing the last non-OK return on the calling thread. */
 const char* gdn_last_error(void);
 

@@ -124,6 +124,58 @@ int gdn_tree_commit(const gdn_dims* dims, const void* meta, const int32_t* accep
   return launch_commit(a, stream);
 }
 
+int gdn_tree_step(const gdn_dims* dims, const void* prev_meta, const int32_t* prev_accepted,
+                  const void* prev_q, const void* prev_k, const void* prev_v, const void* prev_alpha,
+                  const void* prev_beta, int32_t* commit_status, const void* meta, const void* q,
+                  const void* k, const void* v, const void* alpha, const void* beta,
+                  const float* conv_w, const float* conv_state, float* conv_state_out, float* S,
+                  float* out, hipStream_t stream) {
+  int rc = check_dims(dims, "step");
+  if (rc != GDN_OK) return rc;
+  if (dims->B == 0 || dims->T == 0) return GDN_OK;
+  if (!prev_meta || !prev_accepted || !prev_q || !prev_k || !prev_v || !prev_alpha || !prev_beta ||
+      !meta || !q || !k || !v || !alpha || !beta || !conv_w || !conv_state || !conv_state_out || !S ||
+      !out)
+    return set_error(GDN_EINVAL, "step: NULL tensor pointer");
+  const size_t cs_bytes =
+      size_t(dims->B) * 3 * (2 * size_t(dims->Hk) * dims->dk + size_t(dims->Hv) * dims->dv) * sizeof(float);
+  const char* ci = reinterpret_cast<const char*>(conv_state);
+  const char* co = reinterpret_cast<const char*>(conv_state_out);
+  if (ci < co + cs_bytes && co < ci + cs_bytes)
+    return set_error(GDN_EINVAL, "step: conv_state and conv_state_out overlap");
+  VerifyArgs a;
+  a.B = dims->B;
+  a.T = dims->T;
+  a.Hk = dims->Hk;
+  a.Hv = dims->Hv;
+  a.dk = dims->dk;
+  a.dv = dims->dv;
+  a.in_dtype = dims->in_dtype;
+  a.scale = dims->scale > 0.0f ? dims->scale : 1.0f / sqrtf(float(dims->dk));
+  a.meta = meta;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.conv_w = conv_w;
+  a.conv_state = conv_state;
+  a.S0 = S;
+  a.out = out;
+  a.fused = true;
+  a.pmeta = prev_meta;
+  a.paccepted = prev_accepted;
+  a.pq = prev_q;
+  a.pk = prev_k;
+  a.pv = prev_v;
+  a.palpha = prev_alpha;
+  a.pbeta = prev_beta;
+  a.conv_state_out = conv_state_out;
+  a.S = S;
+  a.commit_status = commit_status;
+  return launch_verify(a, stream);
+}
+
 const char* gdn_last_error(void) { return g_err; }
 
 const char* gdn_version(void) { return "gdntree 0.1 (gfx950)"; }

@@ -23,9 +23,7 @@ namespace gdn {
 // threads per state workgroup: 512, or one per state element for tiny heads
 constexpr int commit_threads(int dk, int dv) { return dk * dv >= 512 ? 512 : dk * dv; }
 constexpr int kCMaxT = 128;    // tree slots supported
-constexpr int kMC = 32;        // path nodes featurised per chunk
 constexpr int kMH = kMC / 2;   // path nodes per feature half
-constexpr int kWin = kMH + 3;  // raw conv window of one half
 
 struct CommitParams {
   int B, T, Hk, Hv;
@@ -47,36 +45,6 @@ __device__ __forceinline__ int commit_check(const MetaPtrs& m, int b, int T, int
   if (m.depth[size_t(b) * T + a] < 0) return GDN_TREE_BAD_ACCEPTED;
   return GDN_TREE_OK;
 }
-
-// Inputs of one feature task (a channel over one half of a path chunk).
-// Every load is unconditional (indices clamped) so that nothing waits for
-// it before the features are computed; the conv-state / padding choice is
-// made when the window is used.
-template <typename TIn>
-struct FeatWindow {
-  TIn xr[kWin];  // raw inputs of path nodes m0 - 3 .. m0 + kMH - 1 (clamped)
-  float xc[3];   // conv-state slots 0..2 of the channel
-  float4 w;      // conv weights of the channel
-  __device__ __forceinline__ void load(const TIn* src, size_t stride, const float* cs, size_t cstride,
-                                       const float* wrow, const int* s_path, int m0, int L) {
-#pragma unroll
-    for (int q = 0; q < kWin; ++q) {
-      int mi = m0 - 3 + q;
-      mi = mi < 0 ? 0 : (mi < L ? mi : L - 1);
-      xr[q] = src[size_t(s_path[mi]) * stride];
-    }
-#pragma unroll
-    for (int sl = 0; sl < 3; ++sl) xc[sl] = cs[size_t(sl) * cstride];
-    w = *reinterpret_cast<const float4*>(wrow);
-  }
-  // input of the window element q (path node m0 - 3 + q); the conv-state
-  // slot is picked by selects, not by indexing (keeps xc in registers)
-  __device__ __forceinline__ float x(int q, int m0, int L) const {
-    const int mi = m0 - 3 + q;
-    const float c = mi == -3 ? xc[0] : (mi == -2 ? xc[1] : xc[2]);
-    return mi < 0 ? c : (mi < L ? to_f32(xr[q]) : 0.0f);
-  }
-};
 
 template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(CommitParams p) {
@@ -144,7 +112,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
                           : static_cast<const TIn*>(p.k) + size_t(b) * T * Hk * DK + size_t(g) * DK + fc;
   const size_t fstride = vtask ? size_t(Hv) * DV : size_t(Hk) * DK;
   const float* fcs = p.conv_state + size_t(b) * 3 * C + fch;
-  FeatWindow<TIn> win;
+  FeatWindow<TIn, kMH> win;
   if (vtask || ktask) win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_path, fhalf * kMH, L);
 
   // ---- the state rows load behind the first windows
@@ -204,44 +172,9 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
     }
     __syncthreads();
     const int cnt = L - base < kMC ? L - base : kMC;
-    for (int mr = 0; mr < cnt; ++mr) {
-      const int mi = base + mr;
-      const float al = s_al[mi], be = s_be[mi], inv = s_inv[mr];
-      float kk[EPT];  // un-normalised key; 1 / ||k|| is folded into the scalars
-      if constexpr (EPT % 4 == 0) {
-#pragma unroll
-        for (int e = 0; e < EPT; e += 4) {
-          const float4 x = *reinterpret_cast<const float4*>(&s_fk[mr][col0 + e]);
-          kk[e] = x.x;
-          kk[e + 1] = x.y;
-          kk[e + 2] = x.z;
-          kk[e + 3] = x.w;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) kk[e] = s_fk[mr][col0 + e];
-      }
-      float u0 = 0.0f, u1 = 0.0f;
-#pragma unroll
-      for (int e = 0; e + 1 < EPT; e += 2) {
-        u0 += srow[e] * kk[e];
-        u1 += srow[e + 1] * kk[e + 1];
-      }
-      if (EPT & 1) u0 += srow[EPT - 1] * kk[EPT - 1];
-      const float uu = group_sum<LPR>(u0 + u1) * inv;  // S_stored . k_hat
-      // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
-      // multiplied by 1 / ||k|| so that it applies to the raw key
-      const float ag = al * gamma;
-      const float c = be * (s_fv[mr][row] - ag * uu) * __builtin_amdgcn_rcpf(ag) * inv;
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) srow[e] += c * kk[e];
-      gamma = ag;
-      if (gamma < 0x1p-60f) {  // keep the stored frame in range (uniform branch)
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) srow[e] *= gamma;
-        gamma = 1.0f;
-      }
-    }
+    for (int mr = 0; mr < cnt; ++mr)
+      gamma = replay_step<EPT, LPR>(srow, &s_fk[mr][col0], s_fv[mr][row], s_al[base + mr], s_be[base + mr],
+                                    s_inv[mr], gamma);
     __syncthreads();  // chunk features consumed
   }
   if constexpr (EPT % 4 == 0) {

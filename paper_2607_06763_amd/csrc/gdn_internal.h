@@ -180,6 +180,90 @@ __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const
 }
 
 // ---------------------------------------------------------------------------
+// Commit building blocks shared by the commit kernel and the fused step.
+// ---------------------------------------------------------------------------
+constexpr int kMC = 32;  // path nodes featurised per chunk
+
+// Inputs of one commit feature task: one conv channel over NW consecutive
+// path nodes m0 .. m0 + NW - 1 (the width-4 conv reaches back to m0 - 3;
+// positions above the root read the conv-state slots).  Every load is
+// unconditional (indices clamped) so that nothing waits for it before the
+// features are computed; the conv-state / padding choice is made when the
+// window is used.
+template <typename TIn, int NW>
+struct FeatWindow {
+  static constexpr int kWin = NW + 3;
+  TIn xr[kWin];  // raw inputs of path nodes m0 - 3 .. m0 + NW - 1 (clamped)
+  float xc[3];   // conv-state slots 0..2 of the channel
+  float4 w;      // conv weights of the channel
+  __device__ __forceinline__ void load(const TIn* src, size_t stride, const float* cs, size_t cstride,
+                                       const float* wrow, const int* s_path, int m0, int L) {
+#pragma unroll
+    for (int q = 0; q < kWin; ++q) {
+      int mi = m0 - 3 + q;
+      mi = mi < 0 ? 0 : (mi < L ? mi : L - 1);
+      xr[q] = src[size_t(s_path[mi]) * stride];
+    }
+#pragma unroll
+    for (int sl = 0; sl < 3; ++sl) xc[sl] = cs[size_t(sl) * cstride];
+    w = *reinterpret_cast<const float4*>(wrow);
+  }
+  // input of the window element q (path node m0 - 3 + q); the conv-state
+  // slot is picked by selects, not by indexing (keeps xc in registers)
+  __device__ __forceinline__ float x(int q, int m0, int L) const {
+    const int mi = m0 - 3 + q;
+    const float c = mi == -3 ? xc[0] : (mi == -2 ? xc[1] : xc[2]);
+    return mi < 0 ? c : (mi < L ? to_f32(xr[q]) : 0.0f);
+  }
+};
+
+
+// One rank-1 step of the commit replay on a thread's EPT elements of a state
+// row (LPR lanes per row), Eq. 7 in the stored orientation:
+//   S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T.
+// The row is kept as S = gamma * stored (gamma: running product of alpha),
+// so a step is two FMAs per element; krow is the raw key, inv = 1 / ||k||
+// is folded into the scalars.  Returns the new gamma.
+template <int EPT, int LPR>
+__device__ __forceinline__ float replay_step(float (&sr)[EPT], const float* krow, float vr, float al, float be,
+                                             float inv, float gamma) {
+  float kk[EPT];
+  if constexpr (EPT % 4 == 0) {
+#pragma unroll
+    for (int e = 0; e < EPT; e += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(krow + e);
+      kk[e] = x.x;
+      kk[e + 1] = x.y;
+      kk[e + 2] = x.z;
+      kk[e + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) kk[e] = krow[e];
+  }
+  float u0 = 0.0f, u1 = 0.0f;
+#pragma unroll
+  for (int e = 0; e + 1 < EPT; e += 2) {
+    u0 += sr[e] * kk[e];
+    u1 += sr[e + 1] * kk[e + 1];
+  }
+  if (EPT & 1) u0 += sr[EPT - 1] * kk[EPT - 1];
+  const float uu = group_sum<LPR>(u0 + u1) * inv;  // S_stored . k_hat
+  // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
+  // multiplied by 1 / ||k|| so that it applies to the raw key
+  const float ag = al * gamma;
+  const float c = be * (vr - ag * uu) * __builtin_amdgcn_rcpf(ag) * inv;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) sr[e] += c * kk[e];
+  if (ag < 0x1p-60f) {  // keep the stored frame in range (uniform branch)
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sr[e] *= ag;
+    return 1.0f;
+  }
+  return ag;
+}
+
+// ---------------------------------------------------------------------------
 // Launchers (defined in the kernel sources).  All return a gdn_status value.
 // ---------------------------------------------------------------------------
 int launch_prepare(int B, int T, const int32_t* parent, void* meta, int32_t* tree_status,
@@ -192,6 +276,14 @@ struct VerifyArgs {
   const void *q, *k, *v, *alpha, *beta;
   const float *conv_w, *conv_state, *S0;
   float* out;
+  // fused step (commit of the previous step's accepted path, then verify)
+  bool fused = false;
+  const void* pmeta = nullptr;
+  const int32_t* paccepted = nullptr;
+  const void *pq = nullptr, *pk = nullptr, *pv = nullptr, *palpha = nullptr, *pbeta = nullptr;
+  float* conv_state_out = nullptr;
+  float* S = nullptr;
+  int32_t* commit_status = nullptr;
 };
 int launch_verify(const VerifyArgs& a, hipStream_t stream);
 

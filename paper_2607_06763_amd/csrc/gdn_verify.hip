@@ -61,6 +61,14 @@ struct VerifyParams {
   const void *q, *k, *v, *alpha, *beta;
   const float *conv_w, *conv_state, *S0;
   float* out;
+  // fused step only: the previous step's accepted path is committed into S
+  // (in place; S0 == S) and into conv_state_out before the verification
+  const void* pmeta;
+  const int32_t* paccepted;
+  const void *pq, *pk, *pv, *palpha, *pbeta;
+  float* conv_state_out;
+  float* S;
+  int32_t* commit_status;
 };
 
 // Channel carried in register r (r < D / 8) by lane o (o < 8) of a node:
@@ -167,9 +175,12 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
   const size_t s_tile = size_t(DVS) * (kappa + kSPad) * 2 * 2;  // S0 bf16 hi + lo planes
   s.rv = k_stage > v_tile ? k_stage : v_tile;
   s.rv = s.rv > s_tile ? s.rv : s_tile;
+  const size_t c_tile = size_t(kMC) * (DK + DVS) * 4 + kMC * 4 + 2 * kVMaxT * 4;  // fused commit
+  s.rv = s.rv > c_tile ? s.rv : c_tile;
   s.meta = size_t(3 * kVMaxT) * 4                           // order, parent pos, depth
            + size_t(2 * kVMaxT) * 4                         // alpha, beta of the current head
-           + size_t(8 * DK) * 4 + size_t(4 * DVS) * 4;      // q/k and v conv weights
+           + size_t(8 * DK) * 4 + size_t(4 * DVS) * 4       // q/k and v conv weights
+           + size_t(kVMaxT) * 4;                            // previous path (fused step)
   s.total = s.rk + s.rv + s.meta;
   return s;
 }
@@ -200,22 +211,35 @@ __device__ __forceinline__ void prefetch_v(const TIn* vin, size_t node_stride, c
   }
 }
 
+// Conv-state slot s seen by a step after the commit of a path of L nodes
+// (L = 0: nothing committed): the last three raw inputs of (old slots 0..2,
+// path p_0 .. p_{L-1}), i.e. the old slot L + s while L + s < 3, else the
+// raw input of path node L - 3 + s.
+__device__ __forceinline__ int slot_old(int L, int s) { return L + s < 3 ? L + s : 2; }
+__device__ __forceinline__ bool slot_from_path(int L, int s) { return L + s >= 3; }
+
 // Gates (alpha, beta of the T positions), v conv weights ([4][DVS],
 // tap-major) and v conv-state rows ([3][DVS]) of one value head, loaded
 // into registers ahead of their use.  Every load is unconditional (indices
-// are clamped) so that nothing waits for it before the store.
-template <int DVS, typename TIn>
+// are clamped) so that nothing waits for it before the store.  In the fused
+// step the conv-state rows are those after the commit of the previous path
+// (Lp nodes, path positions in s_ppath, raw values pv of the previous step).
+template <int DVS, typename TIn, bool FUSED>
 struct HeadGates {
   static constexpr int NW = (4 * DVS + kVT - 1) / kVT;
   static constexpr int NC = (3 * DVS + kVT - 1) / kVT;
   TIn al, be;
   float w[NW], cs[NC];
+  TIn cr[FUSED ? NC : 1];  // raw inputs of the committed path (fused step)
+  int Lp = 0;
   __device__ __forceinline__ void load(const TIn* alpha, const TIn* beta, const float* conv_w,
                                        const float* conv_state, const int* s_ord, int b, int T, int Hv,
-                                       int C, int h, int vch0, int tid) {
+                                       int C, int h, int vch0, int tid, const TIn* pv = nullptr,
+                                       size_t vrow = 0, int vcol0 = 0, const int* s_ppath = nullptr, int L = 0) {
     const size_t ab = (size_t(b) * T + s_ord[tid < T ? tid : 0]) * Hv + h;
     al = alpha[ab];
     be = beta[ab];
+    Lp = L;
 #pragma unroll
     for (int j = 0; j < NW; ++j) {
       const int i = j * kVT + tid < 4 * DVS ? j * kVT + tid : 4 * DVS - 1;
@@ -224,7 +248,12 @@ struct HeadGates {
 #pragma unroll
     for (int j = 0; j < NC; ++j) {
       const int i = j * kVT + tid < 3 * DVS ? j * kVT + tid : 3 * DVS - 1;
-      cs[j] = conv_state[(size_t(b) * 3 + i / DVS) * C + vch0 + i % DVS];
+      const int sl = i / DVS;
+      cs[j] = conv_state[(size_t(b) * 3 + slot_old(L, sl)) * C + vch0 + i % DVS];
+      if constexpr (FUSED) {
+        const int node = slot_from_path(L, sl) ? s_ppath[L - 3 + sl] : 0;
+        cr[j] = pv[(size_t(b) * T + node) * vrow + vcol0 + i % DVS];
+      }
     }
   }
   // gates -> s_al, s_be; weights -> s_wv; conv-state rows -> rows T..T+2 of
@@ -241,10 +270,184 @@ struct HeadGates {
 #pragma unroll
     for (int j = 0; j < NC; ++j) {
       const int i = j * kVT + tid;
-      if (i < 3 * DVS) s_v[(T + i / DVS) * vrow + i % DVS] = cs[j];
+      if (i < 3 * DVS) {
+        float x = cs[j];
+        if constexpr (FUSED) x = slot_from_path(Lp, i / DVS) ? to_f32(cr[j]) : x;
+        s_v[(T + i / DVS) * vrow + i % DVS] = x;
+      }
     }
   }
 };
+
+// Split of a DVS x DK state slice over the workgroup for the fused commit:
+// EPT consecutive elements of one row per thread, LPR lanes per row; the
+// first DVS * LPR threads own elements (all of them unless DVS DK < kVT).
+template <int DK, int DVS>
+struct FusedSplit {
+  static constexpr int EPT = DVS * DK >= kVT ? DVS * DK / kVT : 1;
+  static constexpr int LPR = DK / EPT;
+  static_assert(EPT >= 1 && LPR >= 1 && LPR <= 64 && (LPR & (LPR - 1)) == 0, "fused state split");
+  __device__ static __forceinline__ bool owns(int tid) { return tid < DVS * LPR; }
+  __device__ static __forceinline__ int row(int tid) { return owns(tid) ? tid / LPR : DVS - 1; }
+  __device__ static __forceinline__ int col0(int tid) { return (tid % LPR) * EPT; }
+  __device__ static __forceinline__ void load(const float* src, float (&x)[EPT]) {
+    if constexpr (EPT % 4 == 0) {
+#pragma unroll
+      for (int e = 0; e < EPT; e += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(src + e);
+        x[e] = v.x;
+        x[e + 1] = v.y;
+        x[e + 2] = v.z;
+        x[e + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) x[e] = src[e];
+    }
+  }
+  __device__ static __forceinline__ void store(float* dst, const float (&x)[EPT]) {
+    if constexpr (EPT % 4 == 0) {
+#pragma unroll
+      for (int e = 0; e < EPT; e += 4)
+        *reinterpret_cast<float4*>(dst + e) = make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) dst[e] = x[e];
+    }
+  }
+};
+
+// State rows c0 .. c0 + DVS of head h (before the fused commit) in the
+// commit layout.  Threads that own no elements load row 0 (never stored).
+template <int DK, int DVS>
+__device__ __forceinline__ void load_state_rows(const float* S, int b, int Hv, int DV, int h, int c0, int tid,
+                                                float (&sr)[FusedSplit<DK, DVS>::EPT]) {
+  using FS = FusedSplit<DK, DVS>;
+  const int t = FS::owns(tid) ? tid : 0;
+  FS::load(S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(t)) * DK + FS::col0(t), sr);
+}
+
+// Commit (fused step) of the previous step's accepted path (L nodes, slots
+// s_ppath) into the state rows c0 .. c0 + DVS of value head h: features of
+// the path (previous step's raw inputs, conv state before the commit), then
+// one rank-1 step per path node on this thread's elements of the rows
+// (Eq. 7, see replay_step).  sr holds the elements before the commit on
+// entry (load_state_rows) and after it on return; the rows are also stored
+// to S.  Uses lds (the value-tile region) and ends with a barrier; a uniform
+// no-op when L = 0.
+template <int DK, int DVS, typename TIn>
+__device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned char* lds, const int* s_ppath, int L,
+                                             int b, int g, int h, int c0, int tid,
+                                             float (&sr)[FusedSplit<DK, DVS>::EPT]) {
+  using FS = FusedSplit<DK, DVS>;
+  constexpr int EPT = FS::EPT, LPR = FS::LPR;
+  constexpr int FP = 4 * (DK + DVS) <= kVT ? 4 : 2;  // feature parts per chunk
+  constexpr int FN = kMC / FP;                       // path nodes per feature task
+  static_assert(FP * (DK + DVS) <= kVT, "one feature task per thread");
+  if (L == 0) return;
+  const int T = p.T, Hk = p.Hk, Hv = p.Hv, DV = p.DV;
+  const int C = 2 * Hk * DK + Hv * DV;
+  float* s_fk = reinterpret_cast<float*>(lds);  // [kMC][DK] keys (unnormalised)
+  float* s_fv = s_fk + kMC * DK;                // [kMC][DVS] values of the slice
+  float* s_inv = s_fv + kMC * DVS;              // [kMC] 1 / ||k||
+  float* s_al = s_inv + kMC;                    // [kVMaxT] gates by path index
+  float* s_be = s_al + kVMaxT;
+  if (tid < L) {
+    const size_t ab = (size_t(b) * T + s_ppath[tid]) * Hv + h;
+    s_al[tid] = ld(static_cast<const TIn*>(p.palpha), ab);
+    s_be[tid] = ld(static_cast<const TIn*>(p.pbeta), ab);
+  }
+  // feature task of this thread: value channel of the slice (tid < FP DVS)
+  // or key channel (FP DVS <= tid < FP (DVS + DK)); fpart picks the part
+  const bool vtask = tid < FP * DVS;
+  const bool ktask = !vtask && tid < FP * (DVS + DK);
+  const int tt = vtask ? tid : tid - FP * DVS;
+  const int fc = vtask ? tt % DVS : tt % DK;
+  const int fpart = vtask ? tt / DVS : tt / DK;
+  const int fch = vtask ? 2 * Hk * DK + h * DV + c0 + fc : Hk * DK + g * DK + fc;  // conv channel
+  const TIn* fsrc = vtask ? static_cast<const TIn*>(p.pv) + size_t(b) * T * Hv * DV + size_t(h) * DV + c0 + fc
+                          : static_cast<const TIn*>(p.pk) + size_t(b) * T * Hk * DK + size_t(g) * DK + fc;
+  const size_t fstride = vtask ? size_t(Hv) * DV : size_t(Hk) * DK;
+  const float* fcs = p.conv_state + size_t(b) * 3 * C + fch;
+  const int row = FS::row(tid), col0 = FS::col0(tid);
+  float gamma = 1.0f;
+  for (int base = 0; base < L; base += kMC) {
+    FeatWindow<TIn, FN> win;
+    if (vtask || ktask) {
+      const int m0 = base + fpart * FN;
+      win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_ppath, m0, L);
+#pragma unroll
+      for (int mr = 0; mr < FN; ++mr) {
+        const float y = silu(win.w.x * win.x(mr, m0, L) + win.w.y * win.x(mr + 1, m0, L) +
+                             win.w.z * win.x(mr + 2, m0, L) + win.w.w * win.x(mr + 3, m0, L));
+        if (vtask)
+          s_fv[(fpart * FN + mr) * DVS + fc] = y;
+        else
+          s_fk[(fpart * FN + mr) * DK + fc] = y;
+      }
+    }
+    __syncthreads();
+    // key norms: 16 lanes per path node, DK / 16 channels per lane
+    {
+      constexpr int CPL = DK / 16;
+      const int nd = tid >> 4, ln = tid & 15;
+      float ss = 0.0f;
+      if (nd < kMC) {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          const float y = s_fk[nd * DK + ln * CPL + c];
+          ss += y * y;
+        }
+      }
+      ss = group_sum<16>(ss);
+      if (nd < kMC && ln == 0) s_inv[nd] = rsqrt_hw(ss + 1e-6f);
+    }
+    __syncthreads();
+    const int cnt = L - base < kMC ? L - base : kMC;
+    for (int mr = 0; mr < cnt; ++mr)
+      gamma = replay_step<EPT, LPR>(sr, s_fk + mr * DK + col0, s_fv[mr * DVS + row], s_al[base + mr],
+                                    s_be[base + mr], s_inv[mr], gamma);
+    __syncthreads();  // chunk features consumed
+  }
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) sr[e] *= gamma;
+  if (FS::owns(tid)) FS::store(p.S + ((size_t(b) * Hv + h) * DV + c0 + row) * DK + col0, sr);
+}
+
+// Conv state after the fused commit for the channels a workgroup owns:
+// q and k of key head g (if owns_qk) and v of heads h0 .. h0 + hpw - 1,
+// channels c0 .. c0 + DVS.  Slot s is the old slot Lp + s while that is
+// below 3, else the raw input of path node Lp - 3 + s.
+template <int DK, int DVS, typename TIn>
+__device__ __forceinline__ void fused_conv_out(const VerifyParams& p, const int* s_ppath, int L, int b, int g,
+                                               int h0, int c0, bool owns_qk, int tid) {
+  const int T = p.T, Hk = p.Hk, Hv = p.Hv, DV = p.DV;
+  const int C = 2 * Hk * DK + Hv * DV;
+  const float* cs = p.conv_state + size_t(b) * 3 * C;
+  float* co = p.conv_state_out + size_t(b) * 3 * C;
+  if (owns_qk) {
+    const size_t qk_row = size_t(Hk) * DK;
+    for (int i = tid; i < 3 * 2 * DK; i += kVT) {
+      const int sl = i / (2 * DK), part = (i / DK) & 1, c = i % DK;
+      const int ch = part * Hk * DK + g * DK + c;
+      const TIn* src = static_cast<const TIn*>(part ? p.pk : p.pq);
+      const float x = slot_from_path(L, sl) ? ld(src, (size_t(b) * T + s_ppath[L - 3 + sl]) * qk_row + g * DK + c)
+                                            : cs[size_t(slot_old(L, sl)) * C + ch];
+      co[size_t(sl) * C + ch] = x;
+    }
+  }
+  const size_t v_row = size_t(Hv) * DV;
+  const int nv = p.hpw * DVS;
+  for (int i = tid; i < 3 * nv; i += kVT) {
+    const int sl = i / nv, j = i % nv;
+    const int col = (h0 + j / DVS) * DV + c0 + j % DVS;
+    const int ch = 2 * Hk * DK + col;
+    const float x = slot_from_path(L, sl)
+                        ? ld(static_cast<const TIn*>(p.pv), (size_t(b) * T + s_ppath[L - 3 + sl]) * v_row + col)
+                        : cs[size_t(slot_old(L, sl)) * C + ch];
+    co[size_t(sl) * C + ch] = x;
+  }
+}
 
 // Write one 16-byte chunk of raw inputs (8 bf16 or 4 fp32) to LDS as fp32.
 __device__ __forceinline__ void store_chunk_f32(float* dst, uint4 u, const BF16*) {
@@ -258,7 +461,7 @@ __device__ __forceinline__ void store_chunk_f32(float* dst, uint4 u, const float
       make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
 }
 
-template <int DK, int DVS, typename TIn>
+template <int DK, int DVS, typename TIn, bool FUSED>
 __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr int KPL = DK / kLPN;              // key channels per lane and node
@@ -269,7 +472,8 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   constexpr int NT = DVS / 16;                // 16-row value tiles of this slice
   constexpr int VROW = DVS + kKPad;           // v~ / staging row stride (floats)
   constexpr int EPC = 16 / sizeof(TIn);
-  constexpr int NS0 = (DVS * DK / 4 + kVT - 1) / kVT;        // S0 float4 per thread
+  constexpr int NS0 = FUSED ? 1 : (DVS * DK / 4 + kVT - 1) / kVT;  // S0 float4 per thread
+  constexpr int NSR = FUSED ? FusedSplit<DK, DVS>::EPT : 1;       // state floats per thread (fused)
   constexpr int NVC = (kVMaxT * DVS / EPC + kVT - 1) / kVT;  // raw-v chunks per thread
   constexpr int QCPR = DK / EPC;                             // raw q/k chunks per row
   constexpr int NQC = (kVMaxT * QCPR + kVT - 1) / kVT;       // raw q (or k) chunks per thread
@@ -311,11 +515,44 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   float* s_be = s_al + kVMaxT;
   float* s_wqk = s_be + kVMaxT;  // [2][4][DK] tap-major
   float* s_wv = s_wqk + 8 * DK;  // [4][DVS] tap-major
+  int* s_ppath = reinterpret_cast<int*>(s_wv + 4 * DVS);  // previous accepted path (fused step)
 
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
   const int status = m.status[b];
   const int nv = m.nvalid[b];
+  // fused step: the previous step's accepted path root..a (Lp nodes, slot
+  // s_ppath[j] at depth j) is read off a's ancestor bitmask; Lp = 0 when
+  // nothing is committed (accepted -1 or a non-zero commit status)
+  int Lp = 0;
+  float sr[NSR];  // fused step: this thread's state elements of the current head
+  if constexpr (FUSED) {
+    const MetaPtrs pm = meta_ptrs(p.pmeta, p.B, T);
+    const int pa = p.paccepted[b];
+    const int pst = pm.status[b];
+    int cst = pst != GDN_TREE_OK ? pst : (pa >= -1 && pa < T ? GDN_TREE_OK : GDN_TREE_BAD_ACCEPTED);
+    if (cst == GDN_TREE_OK && pa >= 0) {
+      const int da = pm.depth[size_t(b) * T + pa];
+      if (da < 0) cst = GDN_TREE_BAD_ACCEPTED;
+      else Lp = da + 1;
+    }
+    if (tid < kVMaxT) s_ppath[tid] = 0;  // every path index stays a valid slot
+    __syncthreads();
+    if (Lp > 0 && tid < T) {
+      const uint64_t word = pm.anc[(size_t(b) * T + pa) * pm.W + (tid >> 6)];
+      const int dj = pm.depth[size_t(b) * T + tid];
+      if ((tid == pa || ((word >> (tid & 63)) & 1ull)) && dj >= 0 && dj < Lp) s_ppath[dj] = tid;
+    }
+    if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0 && p.commit_status) p.commit_status[b] = cst;
+    __syncthreads();
+  }
   if (status != GDN_TREE_OK) {
+    if constexpr (FUSED) {  // the previous path is committed all the same
+      for (int hh = 0; hh < p.hpw; ++hh) {
+        load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0 + hh, c0, tid, sr);
+        fused_commit<DK, DVS, TIn>(p, s_rv, s_ppath, Lp, b, g, h0 + hh, c0, tid, sr);
+      }
+      fused_conv_out<DK, DVS, TIn>(p, s_ppath, Lp, b, g, h0, c0, blockIdx.x == 0 && blockIdx.y % nhg == 0, tid);
+    }
     for (int hh = 0; hh < p.hpw; ++hh)
       for (int idx = tid; idx < T * DVS; idx += kVT) {
         const int i = idx / DVS, c = idx % DVS;
@@ -343,7 +580,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   const TIn* beta = static_cast<const TIn*>(p.beta);
   float4 s0pf[NS0];
   uint4 vpf[NVC];
-  HeadGates<DVS, TIn> gpf;
+  HeadGates<DVS, TIn, FUSED> gpf;
 
   // ---------------- phase 1: q~ and k~ ----------------
   // Raw rows are staged in LDS as fp32, in canonical order, followed by the
@@ -370,17 +607,31 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     const float* csq = p.conv_state + size_t(b) * 3 * C + g * DK;
     constexpr int NQS = (3 * DK + kVT - 1) / kVT;
     float cq[NQS], ck[NQS];
+    TIn cqr[FUSED ? NQS : 1], ckr[FUSED ? NQS : 1];  // fused step: raw inputs of the committed path
 #pragma unroll
     for (int j = 0; j < NQS; ++j) {
       const int i = j * kVT + tid < 3 * DK ? j * kVT + tid : 3 * DK - 1;
-      cq[j] = csq[size_t(i / DK) * C + i % DK];
-      ck[j] = csq[size_t(i / DK) * C + Hk * DK + i % DK];
+      const int sl = i / DK;
+      cq[j] = csq[size_t(slot_old(Lp, sl)) * C + i % DK];
+      ck[j] = csq[size_t(slot_old(Lp, sl)) * C + Hk * DK + i % DK];
+      if constexpr (FUSED) {
+        const int node = slot_from_path(Lp, sl) ? s_ppath[Lp - 3 + sl] : 0;
+        const size_t off = (size_t(b) * T + node) * qk_row + size_t(g) * DK + i % DK;
+        cqr[j] = static_cast<const TIn*>(p.pq)[off];
+        ckr[j] = static_cast<const TIn*>(p.pk)[off];
+      }
     }
     // the first head's inputs load while q and k are staged: raw v, gates,
     // conv state, then S0 (issued last, waited for last)
     prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, tid, vpf);
-    gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid);
-    prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
+    if constexpr (FUSED) {
+      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid,
+               static_cast<const TIn*>(p.pv), orow, h0 * DV + c0, s_ppath, Lp);
+      load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0, c0, tid, sr);
+    } else {
+      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid);
+      prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
+    }
 #pragma unroll
     for (int j = 0; j < NQC; ++j) {
       const int idx = j * kVT + tid;
@@ -394,8 +645,15 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     for (int j = 0; j < NQS; ++j) {
       const int i = j * kVT + tid;
       if (i < 3 * DK) {
-        s_k[(T + i / DK) * KROW + i % DK] = cq[j];
-        s_kst[(T + i / DK) * KROW + i % DK] = ck[j];
+        float xq = cq[j], xk = ck[j];
+        if constexpr (FUSED) {
+          if (slot_from_path(Lp, i / DK)) {
+            xq = to_f32(cqr[j]);
+            xk = to_f32(ckr[j]);
+          }
+        }
+        s_k[(T + i / DK) * KROW + i % DK] = xq;
+        s_kst[(T + i / DK) * KROW + i % DK] = xk;
       }
     }
   }
@@ -462,6 +720,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   const int sbase = kLPN * (l16 & 7);
   for (int hh = 0; hh < p.hpw; ++hh) {
     const int h = h0 + hh;
+    // fused step: commit the previous path into this head's state rows (sr
+    // then holds the state the tree is verified against)
+    if constexpr (FUSED) fused_commit<DK, DVS, TIn>(p, s_rv, s_ppath, Lp, b, g, h, c0, tid, sr);
     // 2a: raw v rows (prefetched) + 3 conv-state rows -> LDS as fp32
     //     [T + 3][VROW]; gates and v conv weights -> LDS
     const int vch0 = 2 * Hk * DK + h * DV + c0;  // conv channel of v[h][c0]
@@ -603,8 +864,31 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     {
       uint16_t* s_hi = reinterpret_cast<uint16_t*>(s_rv);
       uint16_t* s_lo = s_hi + DVS * (KAPPA + kSPad);
+      if constexpr (FUSED) {
+        using FS = FusedSplit<DK, DVS>;
+        if (FS::owns(tid)) {
+          const int off = FS::row(tid) * (KAPPA + kSPad) + FS::col0(tid);
+          if constexpr (NSR % 4 == 0) {
 #pragma unroll
-      for (int j = 0; j < NS0; ++j) {
+            for (int e = 0; e < NSR; e += 4) {
+              uint2 hi, lo2;
+              split4(make_float4(sr[e], sr[e + 1], sr[e + 2], sr[e + 3]), hi, lo2);
+              *reinterpret_cast<uint2*>(s_hi + off + e) = hi;
+              *reinterpret_cast<uint2*>(s_lo + off + e) = lo2;
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < NSR; ++e) {
+              const uint32_t u = __float_as_uint(sr[e]);
+              const uint32_t hb = u & 0xffff0000u;
+              s_hi[off + e] = uint16_t(hb >> 16);
+              s_lo[off + e] = uint16_t(__float_as_uint(sr[e] - __uint_as_float(hb)) >> 16);
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < NS0 && !FUSED; ++j) {
         const int idx = j * kVT + tid;
         if (NS0 * kVT == DVS * DK / 4 || idx < DVS * DK / 4) {
           const int row = idx / (DK / 4), kch = idx % (DK / 4);
@@ -628,8 +912,14 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     // it in flight
     if (hh + 1 < p.hpw) {
       prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
-      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
-      prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, tid, s0pf);
+      if constexpr (FUSED) {
+        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
+                 static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
+        load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
+      } else {
+        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
+        prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, tid, s0pf);
+      }
     }
     __syncthreads();
 
@@ -659,9 +949,11 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     }
     __syncthreads();  // S0 planes consumed before the next head reuses the region
   }
+  if constexpr (FUSED)
+    fused_conv_out<DK, DVS, TIn>(p, s_ppath, Lp, b, g, h0, c0, blockIdx.x == 0 && blockIdx.y % nhg == 0, tid);
 }
 
-template <int DK, int DVS, typename TIn>
+template <int DK, int DVS, typename TIn, bool FUSED>
 static int launch_verify_t(const VerifyArgs& a, int hpw, int ns, hipStream_t stream) {
   VerifyParams p;
   p.B = a.B;
@@ -681,10 +973,20 @@ static int launch_verify_t(const VerifyArgs& a, int hpw, int ns, hipStream_t str
   p.conv_state = a.conv_state;
   p.S0 = a.S0;
   p.out = a.out;
+  p.pmeta = a.pmeta;
+  p.paccepted = a.paccepted;
+  p.pq = a.pq;
+  p.pk = a.pk;
+  p.pv = a.pv;
+  p.palpha = a.palpha;
+  p.pbeta = a.pbeta;
+  p.conv_state_out = a.conv_state_out;
+  p.S = a.S;
+  p.commit_status = a.commit_status;
   const size_t smem = verify_smem(a.T, DK, DVS).total;
   static bool attr_done = false;
   if (!attr_done) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&verify_kernel<DK, DVS, TIn>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&verify_kernel<DK, DVS, TIn, FUSED>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        int(verify_smem(kVMaxT, DK, DVS).total));
     if (e != hipSuccess)
@@ -692,7 +994,7 @@ static int launch_verify_t(const VerifyArgs& a, int hpw, int ns, hipStream_t str
     attr_done = true;
   }
   const int G = a.Hv / a.Hk;
-  hipLaunchKernelGGL((verify_kernel<DK, DVS, TIn>), dim3(ns, a.Hk * (G / hpw), a.B), dim3(kVT), smem,
+  hipLaunchKernelGGL((verify_kernel<DK, DVS, TIn, FUSED>), dim3(ns, a.Hk * (G / hpw), a.B), dim3(kVT), smem,
                      stream, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify launch: %s", hipGetErrorString(e));
@@ -710,11 +1012,20 @@ static int dispatch_dvs(const VerifyArgs& a, hipStream_t s) {
     hpw = 1;
     while (size_t(a.B) * a.Hv * ns < 256 && a.dv / (2 * ns) >= 32) ns *= 2;
   }
-  switch (a.dv / ns) {
-    case 16: return launch_verify_t<DK, 16, TIn>(a, hpw, ns, s);
-    case 32: return launch_verify_t<DK, 32, TIn>(a, hpw, ns, s);
-    case 64: return launch_verify_t<DK, 64, TIn>(a, hpw, ns, s);
-    case 128: return launch_verify_t<DK, 128, TIn>(a, hpw, ns, s);
+  if (a.fused) {
+    switch (a.dv / ns) {
+      case 16: return launch_verify_t<DK, 16, TIn, true>(a, hpw, ns, s);
+      case 32: return launch_verify_t<DK, 32, TIn, true>(a, hpw, ns, s);
+      case 64: return launch_verify_t<DK, 64, TIn, true>(a, hpw, ns, s);
+      case 128: return launch_verify_t<DK, 128, TIn, true>(a, hpw, ns, s);
+    }
+  } else {
+    switch (a.dv / ns) {
+      case 16: return launch_verify_t<DK, 16, TIn, false>(a, hpw, ns, s);
+      case 32: return launch_verify_t<DK, 32, TIn, false>(a, hpw, ns, s);
+      case 64: return launch_verify_t<DK, 64, TIn, false>(a, hpw, ns, s);
+      case 128: return launch_verify_t<DK, 128, TIn, false>(a, hpw, ns, s);
+    }
   }
   return set_error(GDN_EUNSUPPORTED, "verify: dv=%d unsupported", a.dv);
 }

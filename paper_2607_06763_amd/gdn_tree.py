@@ -20,7 +20,7 @@ TREE_OK, TREE_NO_ROOT, TREE_MULTI_ROOT, TREE_BAD_PARENT, TREE_CYCLE, TREE_BAD_AC
 MAX_T = 128
 
 EXPORTS = ("gdn_tree_meta_bytes", "gdn_tree_prepare", "gdn_tree_verify", "gdn_tree_commit",
-           "gdn_last_error", "gdn_version")
+           "gdn_tree_step", "gdn_last_error", "gdn_version")
 
 
 class GdnError(RuntimeError):
@@ -67,6 +67,8 @@ def lib() -> ctypes.CDLL:
         L.gdn_tree_verify.argtypes = [ctypes.POINTER(Dims)] + [vp] * 11
         L.gdn_tree_commit.restype = ctypes.c_int
         L.gdn_tree_commit.argtypes = [ctypes.POINTER(Dims)] + [vp] * 12
+        L.gdn_tree_step.restype = ctypes.c_int
+        L.gdn_tree_step.argtypes = [ctypes.POINTER(Dims)] + [vp] * 20
         L.gdn_last_error.restype = ctypes.c_char_p
         L.gdn_last_error.argtypes = []
         L.gdn_version.restype = ctypes.c_char_p
@@ -165,6 +167,32 @@ def commit(d: Dims, meta, accepted, q, k, v, alpha, beta, conv_w, conv_state, S,
         _stream(stream)))
 
 
+def step(d: Dims, prev_meta, prev_accepted, prev_q, prev_k, prev_v, prev_alpha, prev_beta,
+         commit_status, meta, q, k, v, alpha, beta, conv_w, conv_state, conv_state_out, S, out,
+         stream=None) -> None:
+    """gdn_tree_step: commit of the previous step's accepted node, then
+    verification of the current tree; S is updated in place, the committed
+    conv state goes to conv_state_out (conv_state is read-only)."""
+    import torch
+    f32, it = torch.float32, _in_dtype(d)
+    mb = (meta_bytes(d.B, d.T),)
+    qk, vs, gs = (d.B, d.T, d.Hk, d.dk), (d.B, d.T, d.Hv, d.dv), (d.B, d.T, d.Hv)
+    _check(lib().gdn_tree_step(
+        ctypes.byref(d), _ptr(prev_meta, mb, torch.uint8, "prev_meta"),
+        _ptr(prev_accepted, (d.B,), torch.int32, "prev_accepted"),
+        _ptr(prev_q, qk, it, "prev_q"), _ptr(prev_k, qk, it, "prev_k"),
+        _ptr(prev_v, vs, it, "prev_v"), _ptr(prev_alpha, gs, it, "prev_alpha"),
+        _ptr(prev_beta, gs, it, "prev_beta"),
+        _ptr(commit_status, (d.B,), torch.int32, "commit_status", allow_none=True),
+        _ptr(meta, mb, torch.uint8, "meta"), _ptr(q, qk, it, "q"), _ptr(k, qk, it, "k"),
+        _ptr(v, vs, it, "v"), _ptr(alpha, gs, it, "alpha"), _ptr(beta, gs, it, "beta"),
+        _ptr(conv_w, (d.C, 4), f32, "conv_w"),
+        _ptr(conv_state, (d.B, 3, d.C), f32, "conv_state"),
+        _ptr(conv_state_out, (d.B, 3, d.C), f32, "conv_state_out"),
+        _ptr(S, (d.B, d.Hv, d.dv, d.dk), f32, "S"),
+        _ptr(out, (d.B, d.T, d.Hv, d.dv), f32, "out"), _stream(stream)))
+
+
 # ---------------------------------------------------------------------------
 # workload upload (host arrays -> device tensors)
 # ---------------------------------------------------------------------------
@@ -207,6 +235,14 @@ class DeviceTree:
         commit(self.dims, self.meta, self.accepted if accepted is None else accepted, self.q,
                self.k, self.v, self.alpha, self.beta, self.conv_w, conv_state, S,
                self.commit_status, stream)
+
+    def step_from(self, prev: "DeviceTree", S, conv_state, conv_state_out, out=None,
+                  accepted=None, stream=None):
+        """Fused step: commit prev's accepted node, then verify this tree."""
+        step(self.dims, prev.meta, prev.accepted if accepted is None else accepted, prev.q,
+             prev.k, prev.v, prev.alpha, prev.beta, prev.commit_status, self.meta, self.q,
+             self.k, self.v, self.alpha, self.beta, self.conv_w, conv_state, conv_state_out, S,
+             self.out if out is None else out, stream)
 
     def meta_arrays(self):
         """Host views of the metadata blob (layout of gdn_tree.h)."""

@@ -90,6 +90,33 @@ def test_host_validation_errors(L):
     assert L.gdn_tree_prepare(ctypes.byref(empty), None, None, None, None) == G.GDN_OK
 
 
+def _call_step(L, d, ptrs):
+    return L.gdn_tree_step(ctypes.byref(d), *[ctypes.c_void_p(x) if x else None for x in ptrs],
+                           None)
+
+
+def test_step_host_validation(L):
+    d = G.make_dims(2, 7, 2, 2, 16, 16, "f32")
+    good = [0x1000 * (i + 1) for i in range(19)]   # never dereferenced on these paths
+    for i in range(19):
+        if i == 7:          # commit_status may be NULL
+            continue
+        ptrs = list(good)
+        ptrs[i] = 0
+        assert _call_step(L, d, ptrs) == G.GDN_EINVAL, i
+        assert "NULL" in G.last_error()
+    # conv_state (index 15) and conv_state_out (16) must not overlap
+    cs_bytes = 2 * 3 * d.C * 4
+    ptrs = list(good)
+    ptrs[15], ptrs[16] = 0x100000, 0x100000 + cs_bytes - 16
+    assert _call_step(L, d, ptrs) == G.GDN_EINVAL
+    assert "overlap" in G.last_error()
+    # shape errors come first; empty problems succeed without touching pointers
+    assert _call_step(L, G.make_dims(1, 7, 2, 3, 16, 16), good) == G.GDN_EINVAL
+    assert _call_step(L, G.make_dims(1, 200, 2, 2, 16, 16), good) == G.GDN_EUNSUPPORTED
+    assert _call_step(L, G.make_dims(0, 7, 2, 2, 16, 16), [0] * 19) == G.GDN_OK
+
+
 def test_binding_rejects_host_tensors(L):
     import torch
     d = G.make_dims(1, 7, 2, 2, 16, 16, "f32")
