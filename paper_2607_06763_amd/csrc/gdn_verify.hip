@@ -327,14 +327,32 @@ __device__ __forceinline__ void load_state_rows(const float* S, int b, int Hv, i
   FS::load(S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(t)) * DK + FS::col0(t), sr);
 }
 
+// Stores float4 groups [j0, j1) of this thread's state elements to the rows
+// of head h (all elements when EPT is not a multiple of 4 and j0 == 0).
+template <int DK, int DVS>
+__device__ __forceinline__ void store_state_rows(float* S, int b, int Hv, int DV, int h, int c0, int tid,
+                                                 const float (&sr)[FusedSplit<DK, DVS>::EPT], int j0, int j1) {
+  using FS = FusedSplit<DK, DVS>;
+  if (!FS::owns(tid)) return;
+  float* dst = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(tid)) * DK + FS::col0(tid);
+  if constexpr (FS::EPT % 4 == 0) {
+#pragma unroll
+    for (int j = 0; j < FS::EPT / 4; ++j)
+      if (j >= j0 && j < j1)
+        *reinterpret_cast<float4*>(dst + 4 * j) = make_float4(sr[4 * j], sr[4 * j + 1], sr[4 * j + 2], sr[4 * j + 3]);
+  } else {
+    if (j0 == 0) FS::store(dst, sr);
+  }
+}
+
 // Commit (fused step) of the previous step's accepted path (L nodes, slots
 // s_ppath) into the state rows c0 .. c0 + DVS of value head h: features of
 // the path (previous step's raw inputs, conv state before the commit), then
 // one rank-1 step per path node on this thread's elements of the rows
 // (Eq. 7, see replay_step).  sr holds the elements before the commit on
-// entry (load_state_rows) and after it on return; the rows are also stored
-// to S.  Uses lds (the value-tile region) and ends with a barrier; a uniform
-// no-op when L = 0.
+// entry (load_state_rows) and after it on return; the caller stores them
+// (store_state_rows).  Uses lds (the value-tile region) and ends with a
+// barrier; a uniform no-op when L = 0.
 template <int DK, int DVS, typename TIn>
 __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned char* lds, const int* s_ppath, int L,
                                              int b, int g, int h, int c0, int tid,
@@ -352,11 +370,11 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
   float* s_inv = s_fv + kMC * DVS;              // [kMC] 1 / ||k||
   float* s_al = s_inv + kMC;                    // [kVMaxT] gates by path index
   float* s_be = s_al + kVMaxT;
-  if (tid < L) {
-    const size_t ab = (size_t(b) * T + s_ppath[tid]) * Hv + h;
-    s_al[tid] = ld(static_cast<const TIn*>(p.palpha), ab);
-    s_be[tid] = ld(static_cast<const TIn*>(p.pbeta), ab);
-  }
+  // gates of path node tid (tid < L; clamped loads, stored with the first
+  // chunk's features so that one wait covers both)
+  const size_t gab = (size_t(b) * T + s_ppath[tid < L ? tid : 0]) * Hv + h;
+  const TIn gal = static_cast<const TIn*>(p.palpha)[gab];
+  const TIn gbe = static_cast<const TIn*>(p.pbeta)[gab];
   // feature task of this thread: value channel of the slice (tid < FP DVS)
   // or key channel (FP DVS <= tid < FP (DVS + DK)); fpart picks the part
   const bool vtask = tid < FP * DVS;
@@ -373,9 +391,13 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
   float gamma = 1.0f;
   for (int base = 0; base < L; base += kMC) {
     FeatWindow<TIn, FN> win;
+    if (vtask || ktask) win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_ppath, base + fpart * FN, L);
+    if (base == 0 && tid < L) {
+      s_al[tid] = to_f32(gal);
+      s_be[tid] = to_f32(gbe);
+    }
     if (vtask || ktask) {
       const int m0 = base + fpart * FN;
-      win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_ppath, m0, L);
 #pragma unroll
       for (int mr = 0; mr < FN; ++mr) {
         const float y = silu(win.w.x * win.x(mr, m0, L) + win.w.y * win.x(mr + 1, m0, L) +
@@ -411,7 +433,6 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
   }
 #pragma unroll
   for (int e = 0; e < EPT; ++e) sr[e] *= gamma;
-  if (FS::owns(tid)) FS::store(p.S + ((size_t(b) * Hv + h) * DV + c0 + row) * DK + col0, sr);
 }
 
 // Conv state after the fused commit for the channels a workgroup owns:
@@ -550,6 +571,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       for (int hh = 0; hh < p.hpw; ++hh) {
         load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0 + hh, c0, tid, sr);
         fused_commit<DK, DVS, TIn>(p, s_rv, s_ppath, Lp, b, g, h0 + hh, c0, tid, sr);
+        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h0 + hh, c0, tid, sr, 0, NSR);
       }
       fused_conv_out<DK, DVS, TIn>(p, s_ppath, Lp, b, g, h0, c0, blockIdx.x == 0 && blockIdx.y % nhg == 0, tid);
     }
@@ -744,6 +766,8 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     {
       int trow[2][4];  // recomputed per head: fewer registers held across heads
       conv_rows(s_dep, s_ppos, T, pos, act, trow);
+      if constexpr (FUSED)
+        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h, c0, tid, sr, 0, NSR);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
