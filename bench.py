@@ -11,10 +11,14 @@ separate launches, prepare / verify / commit).
 The default workload is the large one: 32 trees of 128 nodes (depth 16),
 16 key / 48 value heads, dk = dv = 128, bf16 inputs, fp32 state.
 
+The timed steps run eagerly first (HIP events around every launch give the
+per-kernel durations), then two consecutive steps are captured in a HIP graph
+and replayed (the tree shapes are fixed, so the pass is captured once); the
+replay time is the step time (--no-graph: the eager time).
+
 Prints ONE JSON line on stdout: throughput in tree nodes verified per second
-per GDN layer, the roofline of the dominant kernel (verify), and the CPU
-oracle's throughput on the same workload.  Per-kernel durations come from HIP
-events recorded on the stream the kernels are launched on.
+per GDN layer, the roofline of the dominant kernel (the fused step, or verify
+with --unfused), and the CPU oracle's throughput on the same workload.
 """
 from __future__ import annotations
 
@@ -132,6 +136,15 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4, help="workload index 0..4 (default: large)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tree-size", type=int, default=0,
+                    help="run the large workload's recipe at this tree size T (16..128) instead of "
+                         "the --config workload")
+    ap.add_argument("--shape", default="large", choices=["large", "chain"],
+                    help="tree shape for --tree-size: the large recipe, or single paths of T nodes")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="time eager launches only (default: after the eager pass, two steps are "
+                         "captured in a HIP graph and the replay time is the step time; per-kernel "
+                         "durations always come from the eager pass)")
     ap.add_argument("--unfused", action="store_true",
                     help="time prepare, verify and commit as three launches (default: prepare + "
                          "the fused commit-then-verify step)")
@@ -157,7 +170,7 @@ def main() -> int:
         import __graft_entry__
         __graft_entry__.build()
     torch.cuda.set_device(0)
-    w = W.make_config(args.config)
+    w = W.make_sweep(args.tree_size, shape=args.shape) if args.tree_size else W.make_config(args.config)
     dt = G.DeviceTree(w, device="cuda:0")
     S = dt.S0.clone()
     cs = dt.conv_state.clone()
@@ -212,6 +225,31 @@ def main() -> int:
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    ms_eager = ms_step
+    reps = 0
+    if args.graph:
+        # two consecutive steps (the metadata / conv-state buffers alternate)
+        # captured once; warm-up launches on the capture stream first
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step(0)
+            step(1)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            step(0)
+            step(1)
+        for _ in range(max(1, args.warmup // 2)):
+            g.replay()
+        torch.cuda.synchronize()
+        reps = max(1, (args.steps + 1) // 2)
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            g.replay()
+        torch.cuda.synchronize()
+        ms_step = (time.perf_counter() - t0) * 1e3 / (2 * reps)
     per = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(nev - 1)] for e in events]) * 1e3
     src_hash = verify_source_hash()
     if fused:
@@ -246,13 +284,15 @@ def main() -> int:
                 / HBM_PEAK_GBS, 4),
         }
     detail["algorithmic_bytes"] = nbytes
+    if args.graph:
+        detail["ms_per_step_eager"] = round(ms_eager, 5)
     detail["verify_source_sha256_16"] = src_hash
     out = {
         "metric": "tree nodes verified/s per GDN layer",
         "value": round(nodes / (ms_step * 1e-3), 1),
         "unit": "nodes/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": 2 * reps if args.graph else args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
         "higher_is_better": True,
@@ -263,8 +303,8 @@ def main() -> int:
         "config": {"workload": f"{w.name}: B={w.B} trees x T={w.T} nodes, Hk={w.Hk} Hv={w.Hv} "
                                f"dk={w.dk} dv={w.dv}, {w.in_dtype} inputs, fp32 state and output",
                    "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)",
-                   "step": "prepare + fused commit/verify" if fused else
-                           "prepare + verify + commit"},
+                   "step": ("prepare + fused commit/verify" if fused else
+                            "prepare + verify + commit") + (", HIP graph replay" if args.graph else "")},
         "roofline": roofline,
         "detail": detail,
     }

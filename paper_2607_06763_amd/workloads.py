@@ -296,3 +296,22 @@ def make_random(seed: int, B: int, T: int, Hk: int, Hv: int, dk: int, dv: int,
                                        shuffle, max_depth) for b in range(B)])
     return make_inputs(f"random{seed}", np.asarray(parent, np.int32), Hk, Hv, dk, dv,
                        in_dtype, ch[1:], _uniform_valid_node)
+
+
+def make_sweep(T: int, B: int = 32, shape: str = "large", seed: int = 0) -> Workload:
+    """The large workload's recipe at another tree size T (16 key / 48 value
+    heads, d = 128, bf16 inputs): shape "large" grows a forced spine of
+    min(16, T - 1) edges, then attaches each further node to a uniformly
+    chosen earlier node of depth <= 15 with fewer than 8 children (depth <= 16);
+    shape "chain" makes every tree a single path of T nodes (depth T - 1)."""
+    ss = np.random.SeedSequence([20270, T, B, 0 if shape == "large" else 1, seed])
+    ch = ss.spawn(10)
+    tree_rng = np.random.default_rng(ch[0])
+    if shape == "large":
+        parent = np.stack([random_depth_capped_tree(tree_rng, T, 15, spine=min(16, T - 1),
+                                                    max_children=8) for _ in range(B)])
+    elif shape == "chain":
+        parent = np.stack([chain_tree(T)] * B)
+    else:
+        raise ValueError(f"unknown sweep shape {shape}")
+    return make_inputs(f"{shape}-T{T}", parent, 16, 48, 128, 128, BF16, ch[1:], _uniform_valid_node)
