@@ -145,6 +145,9 @@ def main() -> int:
                     help="time eager launches only (default: after the eager pass, two steps are "
                          "captured in a HIP graph and the replay time is the step time; per-kernel "
                          "durations always come from the eager pass)")
+    ap.add_argument("--chunked", action="store_true",
+                    help="verify with the chunked-form kernel (Eq. 9-13) instead of the pull-back; "
+                         "implies --unfused")
     ap.add_argument("--unfused", action="store_true",
                     help="time prepare, verify and commit as three launches (default: prepare + "
                          "the fused commit-then-verify step)")
@@ -177,7 +180,7 @@ def main() -> int:
     nbytes = algorithmic_bytes(w)
 
     nodes = w.B * w.T
-    fused = not args.unfused
+    fused = not (args.unfused or args.chunked)
     # two metadata buffers and two conv-state buffers alternate between steps:
     # the fused launch reads the previous tree's metadata and conv state while
     # the current tree's are written
@@ -205,7 +208,7 @@ def main() -> int:
         dt.prepare()
         if ev is not None:
             ev[1].record()
-        dt.verify(S0=S, conv_state=cs)
+        dt.verify(S0=S, conv_state=cs, chunked=args.chunked)
         if ev is not None:
             ev[2].record()
         dt.commit(S, cs)
@@ -257,7 +260,7 @@ def main() -> int:
         kname, kbytes = "step", nbytes["step"]
     else:
         us_prep, us_main, us_com = (float(x) for x in per.mean(0))
-        kname, kbytes = "verify", nbytes["verify"]
+        kname, kbytes = ("verify_chunked" if args.chunked else "verify"), nbytes["verify"]
     p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
     ach = kbytes / (us_main * 1e-6) / 1e9
     traffic = measured_traffic(src_hash, kname)
@@ -304,7 +307,7 @@ def main() -> int:
                                f"dk={w.dk} dv={w.dv}, {w.in_dtype} inputs, fp32 state and output",
                    "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)",
                    "step": ("prepare + fused commit/verify" if fused else
-                            "prepare + verify + commit") + (", HIP graph replay" if args.graph else "")},
+                            "prepare + " + ("chunked " if args.chunked else "") + "verify + commit") + (", HIP graph replay" if args.graph else "")},
         "roofline": roofline,
         "detail": detail,
     }

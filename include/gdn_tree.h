@@ -133,6 +133,23 @@ int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const
                     const void* v, const void* alpha, const void* beta, const float* conv_w,
                     const float* conv_state, const float* S0, float* out, hipStream_t stream);
 
+/* The same verification in the paper's chunked form (Sec. 3.4.1, Eq. 9-13):
+ * per (sequence, value head) the interaction matrices X (strict ancestors,
+ * decayed key-key products scaled by beta) and Y (ancestors and self, decayed
+ * query-key products) are built from Gram products, (I + X) U = beta (V -
+ * a K S0^T) is solved by forward substitution over 16-node blocks (each
+ * diagonal block inverted, the off-diagonal blocks applied as a cascade),
+ * and O = scale (a Q S0^T + Y U).  All dense products run on MFMA with a
+ * bf16 hi/lo split (fp32 accumulation).  Arguments, layouts, outputs and
+ * errors are those of gdn_tree_verify; in addition dk and dv must be 32, 64
+ * or 128 (GDN_EUNSUPPORTED otherwise).  Its cost does not grow with the
+ * depth of the tree, while gdn_tree_verify's grows with the sum of the path
+ * lengths. */
+int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* q, const void* k,
+                            const void* v, const void* alpha, const void* beta,
+                            const float* conv_w, const float* conv_state, const float* S0,
+                            float* out, hipStream_t stream);
+
 /* Commit of the accepted node (Sec. 3.4.2: a single pass replays Eq. 7 along
  * the accepted path and writes the state).
  *   accepted      int32 [B]  accepted slot per sequence, -1 = commit nothing

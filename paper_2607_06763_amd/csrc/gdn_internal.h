@@ -286,6 +286,8 @@ struct VerifyArgs {
   int32_t* commit_status = nullptr;
 };
 int launch_verify(const VerifyArgs& a, hipStream_t stream);
+// the paper's chunked form (Eq. 9-13) of the same verification
+int launch_verify_chunked(const VerifyArgs& a, hipStream_t stream);
 
 struct CommitArgs {
   int B, T, Hk, Hv, dk, dv, in_dtype;

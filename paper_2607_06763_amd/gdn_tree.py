@@ -19,8 +19,9 @@ GDN_F32, GDN_BF16 = 0, 1
 TREE_OK, TREE_NO_ROOT, TREE_MULTI_ROOT, TREE_BAD_PARENT, TREE_CYCLE, TREE_BAD_ACCEPTED = range(6)
 MAX_T = 128
 
-EXPORTS = ("gdn_tree_meta_bytes", "gdn_tree_prepare", "gdn_tree_verify", "gdn_tree_commit",
-           "gdn_tree_step", "gdn_last_error", "gdn_version")
+EXPORTS = ("gdn_tree_meta_bytes", "gdn_tree_prepare", "gdn_tree_verify",
+           "gdn_tree_verify_chunked", "gdn_tree_commit", "gdn_tree_step", "gdn_last_error",
+           "gdn_version")
 
 
 class GdnError(RuntimeError):
@@ -65,6 +66,8 @@ def lib() -> ctypes.CDLL:
         L.gdn_tree_prepare.argtypes = [ctypes.POINTER(Dims), vp, vp, vp, vp]
         L.gdn_tree_verify.restype = ctypes.c_int
         L.gdn_tree_verify.argtypes = [ctypes.POINTER(Dims)] + [vp] * 11
+        L.gdn_tree_verify_chunked.restype = ctypes.c_int
+        L.gdn_tree_verify_chunked.argtypes = [ctypes.POINTER(Dims)] + [vp] * 11
         L.gdn_tree_commit.restype = ctypes.c_int
         L.gdn_tree_commit.argtypes = [ctypes.POINTER(Dims)] + [vp] * 12
         L.gdn_tree_step.restype = ctypes.c_int
@@ -135,11 +138,14 @@ def prepare(d: Dims, parent, meta, tree_status=None, stream=None) -> None:
         _ptr(tree_status, (d.B,), torch.int32, "tree_status", allow_none=True), _stream(stream)))
 
 
-def verify(d: Dims, meta, q, k, v, alpha, beta, conv_w, conv_state, S0, out, stream=None) -> None:
-    """gdn_tree_verify: per-node outputs out fp32 [B][T][Hv][dv]."""
+def verify(d: Dims, meta, q, k, v, alpha, beta, conv_w, conv_state, S0, out, stream=None,
+           chunked: bool = False) -> None:
+    """gdn_tree_verify (or gdn_tree_verify_chunked, the paper's chunked
+    form): per-node outputs out fp32 [B][T][Hv][dv]."""
     import torch
     f32, it = torch.float32, _in_dtype(d)
-    _check(lib().gdn_tree_verify(
+    fn = lib().gdn_tree_verify_chunked if chunked else lib().gdn_tree_verify
+    _check(fn(
         ctypes.byref(d), _ptr(meta, (meta_bytes(d.B, d.T),), torch.uint8, "meta"),
         _ptr(q, (d.B, d.T, d.Hk, d.dk), it, "q"), _ptr(k, (d.B, d.T, d.Hk, d.dk), it, "k"),
         _ptr(v, (d.B, d.T, d.Hv, d.dv), it, "v"), _ptr(alpha, (d.B, d.T, d.Hv), it, "alpha"),
@@ -226,10 +232,10 @@ class DeviceTree:
     def prepare(self, stream=None):
         prepare(self.dims, self.parent, self.meta, self.tree_status, stream)
 
-    def verify(self, S0=None, conv_state=None, out=None, stream=None):
+    def verify(self, S0=None, conv_state=None, out=None, stream=None, chunked=False):
         verify(self.dims, self.meta, self.q, self.k, self.v, self.alpha, self.beta, self.conv_w,
                self.conv_state if conv_state is None else conv_state,
-               self.S0 if S0 is None else S0, self.out if out is None else out, stream)
+               self.S0 if S0 is None else S0, self.out if out is None else out, stream, chunked)
 
     def commit(self, S, conv_state, accepted=None, stream=None):
         commit(self.dims, self.meta, self.accepted if accepted is None else accepted, self.q,

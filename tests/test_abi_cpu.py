@@ -117,6 +117,19 @@ def test_step_host_validation(L):
     assert _call_step(L, G.make_dims(0, 7, 2, 2, 16, 16), [0] * 19) == G.GDN_OK
 
 
+def test_chunked_host_validation(L):
+    d = G.make_dims(1, 7, 2, 2, 16, 16, "f32")
+    p = [ctypes.c_void_p(0x1000)] * 10
+    # head dims outside {32, 64, 128} are refused before any device work
+    assert L.gdn_tree_verify_chunked(ctypes.byref(d), *p, None) == G.GDN_EUNSUPPORTED
+    assert "dk=16" in G.last_error()
+    d2 = G.make_dims(1, 7, 2, 2, 32, 16, "f32")
+    assert L.gdn_tree_verify_chunked(ctypes.byref(d2), *p, None) == G.GDN_EUNSUPPORTED
+    assert L.gdn_tree_verify_chunked(ctypes.byref(d2), *([None] * 10), None) == G.GDN_EINVAL
+    assert L.gdn_tree_verify_chunked(ctypes.byref(G.make_dims(0, 7, 2, 2, 32, 32)), *([None] * 10),
+                                     None) == G.GDN_OK
+
+
 def test_binding_rejects_host_tensors(L):
     import torch
     d = G.make_dims(1, 7, 2, 2, 16, 16, "f32")
