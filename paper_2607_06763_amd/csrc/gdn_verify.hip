@@ -15,9 +15,12 @@
 // The leaf-to-root walk ("query pull-back") is O(depth (2 dk + dv)) vector
 // work per node on the VALU; the one dense product left is
 //     O^T = S0 X~^T + ACC^T      (dv x T, K = dk)
-// per (sequence, value head), which runs on the MFMA units with a bf16 hi/lo
-// split of both operands (three bf16 products per tile, fp32 accumulation,
-// ~1e-5 relative error).
+// per (sequence, value head), which runs on the MFMA units in fp16 with fp32
+// accumulation: each row of S0 is first scaled by a power of two that brings
+// its largest magnitude into [1, 2) (exact, undone on the output row), so any
+// finite state fits the fp16 range; x~ is bounded by |q~| = 1.  The rounding
+// of both operands to 11 significant bits puts the error of this product at
+// ~1e-4 of max|o| on the named workloads.
 //
 // Workgroup = (dv slice, key head g with HPW of its value heads, sequence b),
 // 512 threads.  Wave w owns 16 tree positions of the canonical (depth,
@@ -40,9 +43,10 @@
 //     2a/b   raw v (prefetched) -> LDS, conv + SiLU -> v~ in LDS (fp32)
 //     2c     pull-back with k~, v~ gathered from LDS (8 lanes per node),
 //            move to the MFMA layout
-//     2d     S0 (prefetched) -> LDS as bf16 hi/lo planes; prefetch the next
-//            head's S0, raw v, gates and v conv weights
-//     2e     MFMA O^T = S0 X~^T + ACC^T, store
+//     2d     S0 (prefetched) -> LDS as one fp16 plane of row-scaled values;
+//            prefetch the next head's raw v, gates and v conv weights
+//     2e     MFMA P^T = (D S0) X~^T, O^T = D^-1 P^T + ACC^T, store; prefetch
+//            the next head's S0
 #include "gdn_internal.h"
 
 namespace gdn {
@@ -51,7 +55,7 @@ namespace gdn {
 constexpr int kVT = 512;        // threads per workgroup (8 waves)
 constexpr int kVMaxT = 128;     // tree slots supported = 8 waves x 16 nodes
 constexpr int kKPad = 4;        // fp32 row padding of the k~ and v~ tiles
-constexpr int kSPad = 8;        // bf16 row padding of the S0 planes
+constexpr int kSPad = 8;        // fp16 row padding of the S0 plane
 constexpr int kLPN = 8;         // lanes per node in the conv / pull-back layout
 
 struct VerifyParams {
@@ -160,6 +164,43 @@ __device__ __forceinline__ float lane_gather(float v, int src) {
   return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
 }
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Largest magnitude over aligned groups of N consecutive lanes (N <= 32).
+template <int N>
+__device__ __forceinline__ float group_max(float v) {
+  static_assert(N >= 1 && N <= 32 && (N & (N - 1)) == 0, "group size");
+  if constexpr (N >= 2) v = fmaxf(v, dpp_f<kDppQuadXor1>(v));
+  if constexpr (N >= 4) v = fmaxf(v, dpp_f<kDppQuadXor2>(v));
+  if constexpr (N >= 8) v = fmaxf(v, dpp_f<kDppRowHalfMirror>(v));
+  if constexpr (N >= 16) v = fmaxf(v, dpp_f<kDppRowMirror>(v));
+  if constexpr (N >= 32) v = fmaxf(v, __shfl_xor(v, 16));
+  return v;
+}
+
+// Power-of-two row scale for the fp16 S0 plane: for a row whose largest
+// magnitude is m, scale = 2^-floor(log2 m) puts m into [1, 2) and
+// inv = 1 / scale; both are exact.  Zero (or subnormal) rows keep scale 1;
+// the exponent is clamped so that both factors stay normal floats.
+__device__ __forceinline__ void row_scale(float m, float& scale, float& inv) {
+  int ex = int((__float_as_uint(m) >> 23) & 0xffu);
+  if (ex == 0) {
+    scale = inv = 1.0f;
+    return;
+  }
+  ex = ex > 253 ? 253 : ex;
+  scale = __uint_as_float(uint32_t(254 - ex) << 23);
+  inv = __uint_as_float(uint32_t(ex) << 23);
+}
+
+// 4 floats times a scale -> 4 fp16 (round to nearest even), packed in 8 bytes
+__device__ __forceinline__ uint2 to_f16x4(float4 x, float sc) {
+  const _Float16 h0 = (_Float16)(x.x * sc), h1 = (_Float16)(x.y * sc);
+  const _Float16 h2 = (_Float16)(x.z * sc), h3 = (_Float16)(x.w * sc);
+  return make_uint2(uint32_t(__builtin_bit_cast(uint16_t, h0)) | (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16),
+                    uint32_t(__builtin_bit_cast(uint16_t, h2)) | (uint32_t(__builtin_bit_cast(uint16_t, h3)) << 16));
+}
+
 // LDS regions (bytes) for a tree of T slots, key dim DK and value slice DVS
 struct VerifySmem {
   size_t rk, rv, meta, total;
@@ -172,7 +213,7 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
   s.rk = rows * (DK + kKPad) * 4;                           // q staging [T+3][DK+pad], then k~ [TP][DK+pad]
   const size_t k_stage = rows * (DK + kKPad) * 4;           // k staging [T+3][DK+pad]
   const size_t v_tile = rows * (DVS + kKPad) * 4;           // v staging [T+3][DVS+pad], then v~
-  const size_t s_tile = size_t(DVS) * (kappa + kSPad) * 2 * 2;  // S0 bf16 hi + lo planes
+  const size_t s_tile = size_t(DVS) * (kappa + kSPad) * 2;  // S0 fp16 plane
   s.rv = k_stage > v_tile ? k_stage : v_tile;
   s.rv = s.rv > s_tile ? s.rv : s_tile;
   const size_t c_tile = size_t(kMC) * (DK + DVS) * 4 + kMC * 4 + 2 * kVMaxT * 4;  // fused commit
@@ -180,7 +221,8 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
   s.meta = size_t(3 * kVMaxT) * 4                           // order, parent pos, depth
            + size_t(2 * kVMaxT) * 4                         // alpha, beta of the current head
            + size_t(8 * DK) * 4 + size_t(4 * DVS) * 4       // q/k and v conv weights
-           + size_t(kVMaxT) * 4;                            // previous path (fused step)
+           + size_t(kVMaxT) * 4                             // previous path (fused step)
+           + size_t(kVMaxT) * 4;                            // S0 row scales
   s.total = s.rk + s.rv + s.meta;
   return s;
 }
@@ -537,6 +579,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   float* s_wqk = s_be + kVMaxT;  // [2][4][DK] tap-major
   float* s_wv = s_wqk + 8 * DK;  // [4][DVS] tap-major
   int* s_ppath = reinterpret_cast<int*>(s_wv + 4 * DVS);  // previous accepted path (fused step)
+  float* s_rs = reinterpret_cast<float*>(s_ppath + kVMaxT);  // 1 / row scale of the S0 plane
 
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
   const int status = m.status[b];
@@ -643,17 +686,6 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         ckr[j] = static_cast<const TIn*>(p.pk)[off];
       }
     }
-    // the first head's inputs load while q and k are staged: raw v, gates,
-    // conv state, then S0 (issued last, waited for last)
-    prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, tid, vpf);
-    if constexpr (FUSED) {
-      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid,
-               static_cast<const TIn*>(p.pv), orow, h0 * DV + c0, s_ppath, Lp);
-      load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0, c0, tid, sr);
-    } else {
-      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid);
-      prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
-    }
 #pragma unroll
     for (int j = 0; j < NQC; ++j) {
       const int idx = j * kVT + tid;
@@ -677,6 +709,18 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         s_k[(T + i / DK) * KROW + i % DK] = xq;
         s_kst[(T + i / DK) * KROW + i % DK] = xk;
       }
+    }
+    // the first head's inputs load during the q / k conv (issued once the
+    // q and k rows have arrived, so that they do not queue behind them):
+    // raw v, gates, conv state, then S0 (issued last, waited for last)
+    prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, tid, vpf);
+    if constexpr (FUSED) {
+      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid,
+               static_cast<const TIn*>(p.pv), orow, h0 * DV + c0, s_ppath, Lp);
+      load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0, c0, tid, sr);
+    } else {
+      gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid);
+      prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
     }
   }
   __syncthreads();
@@ -883,57 +927,58 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     }
     __syncthreads();  // v~ consumed
 
-    // 2d: S0 of this head -> LDS as bf16 hi/lo planes [DVS][KAPPA + kSPad]
-    //     (key channels in natural order, 16..31 zero for dk = 16)
+    // 2d: S0 of this head -> LDS as one fp16 plane [DVS][KAPPA + kSPad] of
+    //     row-scaled values (key channels in natural order, 16..31 zero for
+    //     dk = 16); the inverse row scales -> s_rs
     {
-      uint16_t* s_hi = reinterpret_cast<uint16_t*>(s_rv);
-      uint16_t* s_lo = s_hi + DVS * (KAPPA + kSPad);
+      _Float16* s_h = reinterpret_cast<_Float16*>(s_rv);
       if constexpr (FUSED) {
         using FS = FusedSplit<DK, DVS>;
+        float m = 0.0f;
+#pragma unroll
+        for (int e = 0; e < NSR; ++e) m = fmaxf(m, fabsf(sr[e]));
+        m = group_max<FS::LPR>(m);
+        float sc, inv;
+        row_scale(m, sc, inv);
         if (FS::owns(tid)) {
           const int off = FS::row(tid) * (KAPPA + kSPad) + FS::col0(tid);
           if constexpr (NSR % 4 == 0) {
 #pragma unroll
-            for (int e = 0; e < NSR; e += 4) {
-              uint2 hi, lo2;
-              split4(make_float4(sr[e], sr[e + 1], sr[e + 2], sr[e + 3]), hi, lo2);
-              *reinterpret_cast<uint2*>(s_hi + off + e) = hi;
-              *reinterpret_cast<uint2*>(s_lo + off + e) = lo2;
-            }
+            for (int e = 0; e < NSR; e += 4)
+              *reinterpret_cast<uint2*>(s_h + off + e) = to_f16x4(make_float4(sr[e], sr[e + 1], sr[e + 2], sr[e + 3]), sc);
           } else {
 #pragma unroll
-            for (int e = 0; e < NSR; ++e) {
-              const uint32_t u = __float_as_uint(sr[e]);
-              const uint32_t hb = u & 0xffff0000u;
-              s_hi[off + e] = uint16_t(hb >> 16);
-              s_lo[off + e] = uint16_t(__float_as_uint(sr[e] - __uint_as_float(hb)) >> 16);
-            }
+            for (int e = 0; e < NSR; ++e) s_h[off + e] = (_Float16)(sr[e] * sc);
           }
+          if (FS::col0(tid) == 0) s_rs[FS::row(tid)] = inv;
         }
-      }
+      } else {
 #pragma unroll
-      for (int j = 0; j < NS0 && !FUSED; ++j) {
-        const int idx = j * kVT + tid;
-        if (NS0 * kVT == DVS * DK / 4 || idx < DVS * DK / 4) {
-          const int row = idx / (DK / 4), kch = idx % (DK / 4);
-          uint2 hi, lo2;
-          split4(s0pf[j], hi, lo2);
-          *reinterpret_cast<uint2*>(s_hi + row * (KAPPA + kSPad) + 4 * kch) = hi;
-          *reinterpret_cast<uint2*>(s_lo + row * (KAPPA + kSPad) + 4 * kch) = lo2;
+        for (int j = 0; j < NS0; ++j) {
+          const int idx = j * kVT + tid;
+          // DK / 4 consecutive threads hold one row (a power of two <= 32)
+          const float4 x = s0pf[j];
+          float m = fmaxf(fmaxf(fabsf(x.x), fabsf(x.y)), fmaxf(fabsf(x.z), fabsf(x.w)));
+          m = group_max<DK / 4>(m);
+          float sc, inv;
+          row_scale(m, sc, inv);
+          if (NS0 * kVT == DVS * DK / 4 || idx < DVS * DK / 4) {
+            const int row = idx / (DK / 4), kch = idx % (DK / 4);
+            *reinterpret_cast<uint2*>(s_h + row * (KAPPA + kSPad) + 4 * kch) = to_f16x4(x, sc);
+            if (kch == 0) s_rs[row] = inv;
+          }
         }
       }
       if (DK < 32) {
         for (int i = tid; i < DVS * 4; i += kVT) {
           const int row = i / 4, kch = 4 + i % 4;
-          *reinterpret_cast<uint2*>(s_hi + row * (KAPPA + kSPad) + 4 * kch) = make_uint2(0, 0);
-          *reinterpret_cast<uint2*>(s_lo + row * (KAPPA + kSPad) + 4 * kch) = make_uint2(0, 0);
+          *reinterpret_cast<uint2*>(s_h + row * (KAPPA + kSPad) + 4 * kch) = make_uint2(0, 0);
         }
       }
     }
     __builtin_amdgcn_sched_barrier(0);  // this head's S0 registers are free before the next loads
-    // the next head's raw values, gates and S0 load during the MFMA phase;
-    // S0 is issued last, so the wait for the others in the next 2a leaves
-    // it in flight
+    // the next head's raw values and gates (and, fused step, its state rows)
+    // load during the MFMA phase
     if (hh + 1 < p.hpw) {
       prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
       if constexpr (FUSED) {
@@ -942,35 +987,42 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
       } else {
         gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
-        prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, tid, s0pf);
       }
     }
     __syncthreads();
 
-    // 2e: O^T = S0 X~^T + ACC^T on MFMA (MFMA layout); store
+    // 2e: P^T = (D S0) X~^T on MFMA (fp16 operands, fp32 accumulation);
+    //     O^T = scale (D^-1 P^T + ACC^T) in the accumulator layout; store
     {
-      bf16x8 xh[KB], xl[KB];
+      f16x8 xb[KB];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) split8(xm[kb], xh[kb], xl[kb]);
-      const uint16_t* s_hi = reinterpret_cast<const uint16_t*>(s_rv);
-      const uint16_t* s_lo = s_hi + DVS * (KAPPA + kSPad);
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xb[kb][e] = (_Float16)xm[kb][e];
+      const _Float16* s_h = reinterpret_cast<const _Float16*>(s_rv);
       const int node = mpos < T ? s_ord[mpos] : 0;
       float* orow_p = p.out + (size_t(b) * T + node) * orow + size_t(h) * DV + c0;
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        f32x4 d = {am[n][0], am[n][1], am[n][2], am[n][3]};
+        f32x4 d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
           const int off = (16 * n + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg;
-          const bf16x8 ah = *reinterpret_cast<const bf16x8*>(s_hi + off);
-          const bf16x8 al = *reinterpret_cast<const bf16x8*>(s_lo + off);
-          d = mfma3(ah, al, xh[kb], xl[kb], d);
+          const f16x8 a = *reinterpret_cast<const f16x8*>(s_h + off);
+          d = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, xb[kb], d, 0, 0, 0);
         }
+        const float4 rs = *reinterpret_cast<const float4*>(s_rs + 16 * n + 4 * mlg);
         if (mpos < T)
           *reinterpret_cast<float4*>(orow_p + 16 * n + 4 * mlg) =
-              make_float4(d[0] * p.scale, d[1] * p.scale, d[2] * p.scale, d[3] * p.scale);
+              make_float4(p.scale * fmaf(d[0], rs.x, am[n][0]), p.scale * fmaf(d[1], rs.y, am[n][1]),
+                          p.scale * fmaf(d[2], rs.z, am[n][2]), p.scale * fmaf(d[3], rs.w, am[n][3]));
       }
     }
+    // the next head's S0 loads behind this head's output stores; it is
+    // needed only after the next head's conv and pull-back
+    if constexpr (!FUSED)
+      if (hh + 1 < p.hpw)
+        prefetch_s0<DK, DVS, NS0>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, tid, s0pf);
     __syncthreads();  // S0 planes consumed before the next head reuses the region
   }
   if constexpr (FUSED)
