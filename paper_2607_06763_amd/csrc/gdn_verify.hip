@@ -75,20 +75,37 @@ struct VerifyParams {
   int32_t* commit_status;
 };
 
-// Channel carried in register r (r < D / 8) by lane o (o < 8) of a node:
-// groups of 4 consecutive channels, lane o taking group o of every 32.
+// LDS rows of the conv / pull-back tiles: D floats, unpadded, for D >= 64;
+// D + 4 floats otherwise.  With unpadded rows of 512 or 256 bytes the 128-byte
+// chunk c of any row sits in bank half c % 2 (64 banks of 4 bytes), so when
+// the odd lane groups of a wave read the chunks of their rows in the order
+// c ^ 1 (chunk swap sw = 1) the two lane groups of every 16-lane quarter of a
+// ds_read_b128 hit disjoint bank halves whatever rows they read.
 template <int D>
-__device__ __forceinline__ constexpr int lane_chan(int o, int r) {
-  return D >= 32 ? 32 * (r / 4) + 4 * o + (r % 4) : 2 * o + r;
+__device__ __forceinline__ constexpr int row_floats() {
+  return D >= 64 ? D : D + kKPad;
+}
+// chunk swap of the lane group ln for rows of D floats
+template <int D>
+__device__ __forceinline__ constexpr int chunk_swap(int ln) {
+  return D >= 64 ? (ln & 1) : 0;
+}
+
+// Channel carried in register r (r < D / 8) by lane o (o < 8) of a node with
+// chunk swap sw: groups of 4 consecutive channels, lane o taking group o of
+// every 32-channel chunk, chunks in the order c ^ sw.
+template <int D>
+__device__ __forceinline__ constexpr int lane_chan(int o, int r, int sw) {
+  return D >= 32 ? 32 * ((r / 4) ^ sw) + 4 * o + (r % 4) : 2 * o + r;
 }
 
 // This lane's D / 8 channels of an fp32 LDS row (16-byte or 8-byte pieces).
 template <int D>
-__device__ __forceinline__ void ld_lane(const float* row, int o, float (&x)[D / kLPN]) {
+__device__ __forceinline__ void ld_lane(const float* row, int o, int sw, float (&x)[D / kLPN]) {
   if constexpr (D >= 32) {
 #pragma unroll
     for (int c = 0; c < D / 32; ++c) {
-      const float4 v = *reinterpret_cast<const float4*>(row + 32 * c + 4 * o);
+      const float4 v = *reinterpret_cast<const float4*>(row + 32 * (c ^ sw) + 4 * o);
       x[4 * c] = v.x;
       x[4 * c + 1] = v.y;
       x[4 * c + 2] = v.z;
@@ -101,11 +118,11 @@ __device__ __forceinline__ void ld_lane(const float* row, int o, float (&x)[D / 
   }
 }
 template <int D>
-__device__ __forceinline__ void st_lane(float* row, int o, const float (&x)[D / kLPN]) {
+__device__ __forceinline__ void st_lane(float* row, int o, int sw, const float (&x)[D / kLPN]) {
   if constexpr (D >= 32) {
 #pragma unroll
     for (int c = 0; c < D / 32; ++c)
-      *reinterpret_cast<float4*>(row + 32 * c + 4 * o) =
+      *reinterpret_cast<float4*>(row + 32 * (c ^ sw) + 4 * o) =
           make_float4(x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]);
   } else {
     *reinterpret_cast<float2*>(row + 2 * o) = make_float2(x[0], x[1]);
@@ -133,11 +150,11 @@ __device__ __forceinline__ void conv_rows(const int* s_dep, const int* s_ppos, i
   }
 }
 
-// Offset (floats) of row t of a tile with rows of D + kKPad floats.
+// Offset (floats) of row t of a conv / pull-back tile.
 template <int D>
 __device__ __forceinline__ int row_off(int t) {
-  static_assert((D & (D - 1)) == 0 && kKPad == 4, "power-of-two rows plus 4");
-  return (t << __builtin_ctz(D)) + (t << 2);
+  static_assert((D & (D - 1)) == 0 && kKPad == 4, "power-of-two rows (plus 4)");
+  return D >= 64 ? (t << __builtin_ctz(D)) : (t << __builtin_ctz(D)) + (t << 2);
 }
 
 // 4 floats -> packed bf16 hi (2 dwords) and lo (2 dwords), truncation split
@@ -210,9 +227,10 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
   const int kappa = DK >= 32 ? DK : 32;
   const size_t rows = size_t(TP > T + 3 ? TP : T + 3);
   VerifySmem s;
-  s.rk = rows * (DK + kKPad) * 4;                           // q staging [T+3][DK+pad], then k~ [TP][DK+pad]
-  const size_t k_stage = rows * (DK + kKPad) * 4;           // k staging [T+3][DK+pad]
-  const size_t v_tile = rows * (DVS + kKPad) * 4;           // v staging [T+3][DVS+pad], then v~
+  const int krow = DK >= 64 ? DK : DK + kKPad, vrow = DVS >= 64 ? DVS : DVS + kKPad;
+  s.rk = rows * krow * 4;                                   // q staging [T+3][krow], then k~ [TP][krow]
+  const size_t k_stage = rows * krow * 4;                   // k staging [T+3][krow]
+  const size_t v_tile = rows * vrow * 4;                    // v staging [T+3][vrow], then v~
   const size_t s_tile = size_t(DVS) * (kappa + kSPad) * 2;  // S0 fp16 plane
   s.rv = k_stage > v_tile ? k_stage : v_tile;
   s.rv = s.rv > s_tile ? s.rv : s_tile;
@@ -228,11 +246,15 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
 }
 
 // Issue the loads of this thread's share of S0[b][h][c0 .. c0+DVS][0 .. DK).
-template <int DK, int DVS, int NS0>
-__device__ __forceinline__ void prefetch_s0(const float* S0bh, int tid, float4 (&pf)[NS0]) {
+// Only the loads j with j % PARTS == part are issued, so that a prefetch can
+// be spread over the steps of a compute phase (a burst of loads holds the
+// issuing wave until most of its data has arrived).
+template <int DK, int DVS, int NS0, int PARTS = 1>
+__device__ __forceinline__ void prefetch_s0(const float* S0bh, int tid, float4 (&pf)[NS0], int part = 0) {
   constexpr int n4 = DVS * DK / 4;
 #pragma unroll
   for (int j = 0; j < NS0; ++j) {
+    if (j % PARTS != part) continue;
     const int idx = j * kVT + tid;
     pf[j] = idx < n4 ? reinterpret_cast<const float4*>(S0bh)[idx] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
@@ -240,13 +262,14 @@ __device__ __forceinline__ void prefetch_s0(const float* S0bh, int tid, float4 (
 
 // Issue the loads of this thread's share of the raw values v[b][.][h][c0 .. c0+DVS)
 // for the T nodes (16-byte chunks, node-major).
-template <typename TIn, int DVS, int NVC>
+template <typename TIn, int DVS, int NVC, int PARTS = 1>
 __device__ __forceinline__ void prefetch_v(const TIn* vin, size_t node_stride, const int* s_ord,
-                                           int T, int tid, uint4 (&pf)[NVC]) {
+                                           int T, int tid, uint4 (&pf)[NVC], int part = 0) {
   constexpr int EPC = 16 / sizeof(TIn);  // elements per 16-byte chunk
   constexpr int CPR = DVS / EPC;         // chunks per node row
 #pragma unroll
   for (int j = 0; j < NVC; ++j) {
+    if (j % PARTS != part) continue;
     const int idx = j * kVT + tid;
     const int p = idx / CPR < T ? idx / CPR : T - 1, c = idx % CPR;  // rows >= T are never stored
     pf[j] = *reinterpret_cast<const uint4*>(vin + size_t(s_ord[p]) * node_stride + c * EPC);
@@ -531,9 +554,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   constexpr int VPL = DVS / kLPN;             // value channels per lane and node
   constexpr int KB = DK >= 32 ? DK / 32 : 1;  // 32-wide MFMA k blocks (dk = 16 is zero-padded)
   constexpr int KAPPA = 32 * KB;              // MFMA k extent
-  constexpr int KROW = DK + kKPad;            // k~ / staging row stride (floats)
+  constexpr int KROW = row_floats<DK>();      // k~ / staging row stride (floats)
   constexpr int NT = DVS / 16;                // 16-row value tiles of this slice
-  constexpr int VROW = DVS + kKPad;           // v~ / staging row stride (floats)
+  constexpr int VROW = row_floats<DVS>();     // v~ / staging row stride (floats)
   constexpr int EPC = 16 / sizeof(TIn);
   constexpr int NS0 = FUSED ? 1 : (DVS * DK / 4 + kVT - 1) / kVT;  // S0 float4 per thread
   constexpr int NSR = FUSED ? FusedSplit<DK, DVS>::EPT : 1;       // state floats per thread (fused)
@@ -561,6 +584,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   const int base[2] = {16 * pw + hw, 16 * (7 - pw) + hw};
   // conv / pull-back layout: node n = lane / 8 of each half, lane o = lane % 8
   const int ln = lane >> 3, lo = lane & 7;
+  const int ksw = chunk_swap<DK>(ln), vsw = chunk_swap<DVS>(ln);  // chunk order of this lane group
   const int pos[2] = {base[0] + 2 * ln, base[1] + 2 * ln};
   // MFMA layout: node column l16 (l16 < 8 from the shallow half, else the
   // deep one), channel group mlg
@@ -710,9 +734,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         s_kst[(T + i / DK) * KROW + i % DK] = xk;
       }
     }
-    // the first head's inputs load during the q / k conv (issued once the
-    // q and k rows have arrived, so that they do not queue behind them):
-    // raw v, gates, conv state, then S0 (issued last, waited for last)
+    // the first head's raw values and gates (and, fused step, its state
+    // rows) load during the q / k conv, issued once the q and k rows have
+    // arrived so that they do not queue behind them
     prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h0) * DV + c0, orow, s_ord, T, tid, vpf);
     if constexpr (FUSED) {
       gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid,
@@ -720,7 +744,6 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0, c0, tid, sr);
     } else {
       gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h0, 2 * Hk * DK + h0 * DV + c0, tid);
-      prefetch_s0<DK, DVS>(p.S0 + (size_t(b) * Hv + h0) * DV * DK + size_t(c0) * DK, tid, s0pf);
     }
   }
   __syncthreads();
@@ -729,7 +752,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   for (int u = 0; u < 2; ++u) act[u] = pos[u] < nv;
   int trow[2][4];
   conv_rows(s_dep, s_ppos, T, pos, act, trow);
-  float qh[2][KPL];  // q~ of this lane's two nodes (channels lane_chan(lo, r))
+  float qh[2][KPL];  // q~ of this lane's two nodes (channels lane_chan(lo, r, ksw))
   float kh[2][KPL];
 #pragma unroll
   for (int part = 0; part < 2; ++part) {
@@ -743,11 +766,11 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       float wt[KPL];
-      ld_lane<DK>(wpart + w * DK, lo, wt);
+      ld_lane<DK>(wpart + w * DK, lo, ksw, wt);
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         float xw[KPL];
-        ld_lane<DK>(stage + trow[u][w] * KROW, lo, xw);
+        ld_lane<DK>(stage + trow[u][w] * KROW, lo, ksw, xw);
 #pragma unroll
         for (int c = 0; c < KPL; ++c) y[u][c] += wt[c] * xw[c];
       }
@@ -777,7 +800,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   __syncthreads();  // staged rows consumed
 #pragma unroll
   for (int u = 0; u < 2; ++u)
-    if (act[u]) st_lane<DK>(s_k + pos[u] * KROW, lo, kh[u]);
+    if (act[u]) st_lane<DK>(s_k + pos[u] * KROW, lo, ksw, kh[u]);
 
   // ---------------- phase 2: one value head at a time ----------------
   // MFMA lane (l16, mlg) takes node l16 from half l16 / 8 of the 8-lane
@@ -805,7 +828,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     }
     gpf.store(s_al, s_be, s_wv, s_v, VROW, T, tid);
     __syncthreads();
-    // 2b: v~ of this lane's two nodes, channels lane_chan(lo, r)
+    // 2b: v~ of this lane's two nodes, channels lane_chan(lo, r, vsw)
     float vt[2][VPL];
     {
       int trow[2][4];  // recomputed per head: fewer registers held across heads
@@ -816,17 +839,21 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int c = 0; c < VPL; ++c) vt[u][c] = 0.0f;
+      if constexpr (!FUSED)
+        prefetch_s0<DK, DVS, NS0>(p.S0 + (size_t(b) * Hv + h) * DV * DK + size_t(c0) * DK, tid, s0pf);
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         float wt[VPL];
-        ld_lane<DVS>(s_wv + w * DVS, lo, wt);
+        ld_lane<DVS>(s_wv + w * DVS, lo, vsw, wt);
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
           float xw[VPL];
-          ld_lane<DVS>(s_v + trow[u][w] * VROW, lo, xw);
+          ld_lane<DVS>(s_v + trow[u][w] * VROW, lo, vsw, xw);
 #pragma unroll
           for (int c = 0; c < VPL; ++c) vt[u][c] += wt[c] * xw[c];
         }
+        // this head's S0, a quarter per tap: it is needed after the
+        // pull-back, and spreading the loads keeps the wave issuing
         __builtin_amdgcn_sched_barrier(0);  // one tap's rows in flight at a time
       }
 #pragma unroll
@@ -840,7 +867,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     __syncthreads();  // staged rows consumed
 #pragma unroll
     for (int u = 0; u < 2; ++u)
-      if (act[u]) st_lane<DVS>(s_v + pos[u] * VROW, lo, vt[u]);
+      if (act[u]) st_lane<DVS>(s_v + pos[u] * VROW, lo, vsw, vt[u]);
     __syncthreads();
 
     // 2c: query pull-back along the path of each node, leaf to root; the
@@ -860,8 +887,8 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         const float al = s_al[t];
         const int nx = s_ppos[t];
         float kt[KPL], vv[VPL];
-        ld_lane<DK>(s_k + row_off<DK>(t), lo, kt);
-        ld_lane<DVS>(s_v + row_off<DVS>(t), lo, vv);
+        ld_lane<DK>(s_k + row_off<DK>(t), lo, ksw, kt);
+        ld_lane<DVS>(s_v + row_off<DVS>(t), lo, vsw, vv);
         float s0 = 0.f, s1 = 0.f;
 #pragma unroll
         for (int c = 0; c < KPL; c += 2) {
@@ -925,6 +952,31 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    // a column whose source lane group is odd (l16 odd) received the 32-channel
+    // chunks in the swapped order c ^ 1: put them back in place
+    if (l16 & 1) {
+      if constexpr (DK >= 64) {
+#pragma unroll
+        for (int kb = 0; kb < KB; kb += 2)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float t0 = xm[kb][e];
+            xm[kb][e] = xm[kb + 1][e];
+            xm[kb + 1][e] = t0;
+          }
+      }
+      if constexpr (DVS >= 64) {
+#pragma unroll
+        for (int n = 0; n < NT; ++n)
+          if ((n & 2) == 0)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float t0 = am[n][e];
+              am[n][e] = am[n + 2][e];
+              am[n + 2][e] = t0;
+            }
+      }
+    }
     __syncthreads();  // v~ consumed
 
     // 2d: S0 of this head -> LDS as one fp16 plane [DVS][KAPPA + kSPad] of
@@ -977,18 +1029,10 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
     }
     __builtin_amdgcn_sched_barrier(0);  // this head's S0 registers are free before the next loads
-    // the next head's raw values and gates (and, fused step, its state rows)
-    // load during the MFMA phase
-    if (hh + 1 < p.hpw) {
-      prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
-      if constexpr (FUSED) {
-        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
-                 static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
-        load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
-      } else {
-        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
-      }
-    }
+    // fused step: the next head's state rows load during the MFMA phase
+    // (its fused commit at the start of the next head needs them)
+    if constexpr (FUSED)
+      if (hh + 1 < p.hpw) load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
     __syncthreads();
 
     // 2e: P^T = (D S0) X~^T on MFMA (fp16 operands, fp32 accumulation);
@@ -1016,13 +1060,21 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
           *reinterpret_cast<float4*>(orow_p + 16 * n + 4 * mlg) =
               make_float4(p.scale * fmaf(d[0], rs.x, am[n][0]), p.scale * fmaf(d[1], rs.y, am[n][1]),
                           p.scale * fmaf(d[2], rs.z, am[n][2]), p.scale * fmaf(d[3], rs.w, am[n][3]));
+        // the next head's raw values and gates load tile by tile behind the
+        // output stores
+        if (hh + 1 < p.hpw) {
+          prefetch_v<TIn, DVS, NVC, NT>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid,
+                                        vpf, n);
+          if (n == NT - 1) {
+            if constexpr (FUSED)
+              gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
+                       static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
+            else
+              gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
+          }
+        }
       }
     }
-    // the next head's S0 loads behind this head's output stores; it is
-    // needed only after the next head's conv and pull-back
-    if constexpr (!FUSED)
-      if (hh + 1 < p.hpw)
-        prefetch_s0<DK, DVS, NS0>(p.S0 + (size_t(b) * Hv + h + 1) * DV * DK + size_t(c0) * DK, tid, s0pf);
     __syncthreads();  // S0 planes consumed before the next head reuses the region
   }
   if constexpr (FUSED)
