@@ -35,7 +35,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 VERIFY_SOURCES = ("paper_2607_06763_amd/csrc/gdn_verify.hip", "paper_2607_06763_amd/csrc/gdn_internal.h")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "verify_large_hbm_traffic.md")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def verify_source_hash() -> str:
@@ -77,13 +77,15 @@ def algorithmic_bytes(w) -> dict:
             "step": int(fused)}
 
 
-def measured_traffic(src_hash: str, kernel: str):
+def measured_traffic(src_hash: str, kernel: str, workload: str):
     """HBM bytes per launch of kernel from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
-    if not os.path.exists(TRAFFIC_FILE):
+    summary (profiles/<kernel>_<workload>_hbm_traffic.md), if it was taken on
+    the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
         return None
     vals = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line and line.startswith("- "):
                 k, v = line[2:].split(":", 1)
@@ -263,7 +265,7 @@ def main() -> int:
         kname, kbytes = ("verify_chunked" if args.chunked else "verify"), nbytes["verify"]
     p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
     ach = kbytes / (us_main * 1e-6) / 1e9
-    traffic = measured_traffic(src_hash, kname)
+    traffic = measured_traffic(src_hash, kname, w.name)
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": kname, "algorithmic_bytes_per_launch": kbytes,
