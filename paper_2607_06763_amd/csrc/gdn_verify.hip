@@ -1046,31 +1046,46 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       const _Float16* s_h = reinterpret_cast<const _Float16*>(s_rv);
       const int node = mpos < T ? s_ord[mpos] : 0;
       float* orow_p = p.out + (size_t(b) * T + node) * orow + size_t(h) * DV + c0;
+      // two tiles at a time: both tiles' operands are read first and the two
+      // accumulation chains interleave
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        f32x4 d = {0.f, 0.f, 0.f, 0.f};
+      for (int n = 0; n < NT; n += 2) {
+        constexpr int NP = NT > 1 ? 2 : 1;
+        f16x8 a[NP][KB];
+        float4 rs[NP];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          const int off = (16 * n + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg;
-          const f16x8 a = *reinterpret_cast<const f16x8*>(s_h + off);
-          d = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, xb[kb], d, 0, 0, 0);
+        for (int u = 0; u < NP; ++u) {
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb)
+            a[u][kb] = *reinterpret_cast<const f16x8*>(s_h + (16 * (n + u) + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg);
+          rs[u] = *reinterpret_cast<const float4*>(s_rs + 16 * (n + u) + 4 * mlg);
         }
-        const float4 rs = *reinterpret_cast<const float4*>(s_rs + 16 * n + 4 * mlg);
-        if (mpos < T)
-          *reinterpret_cast<float4*>(orow_p + 16 * n + 4 * mlg) =
-              make_float4(p.scale * fmaf(d[0], rs.x, am[n][0]), p.scale * fmaf(d[1], rs.y, am[n][1]),
-                          p.scale * fmaf(d[2], rs.z, am[n][2]), p.scale * fmaf(d[3], rs.w, am[n][3]));
-        // the next head's raw values and gates load tile by tile behind the
-        // output stores
-        if (hh + 1 < p.hpw) {
-          prefetch_v<TIn, DVS, NVC, NT>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid,
-                                        vpf, n);
-          if (n == NT - 1) {
-            if constexpr (FUSED)
-              gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
-                       static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
-            else
-              gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
+        f32x4 d[NP];
+#pragma unroll
+        for (int u = 0; u < NP; ++u) d[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+          for (int u = 0; u < NP; ++u) d[u] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[u][kb], xb[kb], d[u], 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < NP; ++u) {
+          const int t = n + u;
+          if (mpos < T)
+            *reinterpret_cast<float4*>(orow_p + 16 * t + 4 * mlg) =
+                make_float4(p.scale * fmaf(d[u][0], rs[u].x, am[t][0]), p.scale * fmaf(d[u][1], rs[u].y, am[t][1]),
+                            p.scale * fmaf(d[u][2], rs[u].z, am[t][2]), p.scale * fmaf(d[u][3], rs[u].w, am[t][3]));
+          // the next head's raw values and gates load tile by tile behind
+          // the output stores
+          if (hh + 1 < p.hpw) {
+            prefetch_v<TIn, DVS, NVC, NT>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid,
+                                          vpf, t);
+            if (t == NT - 1) {
+              if constexpr (FUSED)
+                gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
+                         static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
+              else
+                gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
+            }
           }
         }
       }
