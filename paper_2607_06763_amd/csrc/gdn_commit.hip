@@ -7,8 +7,9 @@
 // of a chunk of 32 path nodes) slides the width-4 conv window along the path
 // (conv-state slots above the root) into LDS, its raw inputs loaded before
 // the state rows; the key norms are reduced per path node;
-// each row of S[b][h] (dv rows of dk) lives in the registers of LPR lanes and
-// takes one rank-1 step per path node,
+// each row of S[b][h] (dv rows of dk) lives in the registers of LPR lanes
+// (a thread holds pieces of R rows that share the key slice) and takes one
+// rank-1 step per path node,
 //     S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T,
 // which is Eq. 7 in the stored orientation S <- alpha S (I - beta k k^T) + beta v k^T.
 // The rows are kept as S = gamma * S_stored with gamma the running product of
@@ -50,8 +51,11 @@ template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(CommitParams p) {
   constexpr int kCT = commit_threads(DK, DV);
   constexpr int EPT = DV * DK / kCT;  // state elements per thread
-  constexpr int LPR = DK / EPT;       // lanes per state row (power of 2)
-  static_assert(EPT >= 1 && (EPT < 4 || EPT % 4 == 0), "state split");
+  constexpr int R = EPT >= 16 ? 2 : 1;  // rows per thread (rows q and q + RS)
+  constexpr int CPT = EPT / R;          // columns per thread and row
+  constexpr int LPR = DK / CPT;         // lanes per state row (power of 2)
+  constexpr int RS = DV / R;
+  static_assert(EPT >= 1 && (EPT < 4 || EPT % 4 == 0) && DV % R == 0, "state split");
   static_assert(LPR >= 1 && LPR <= 32 && (LPR & (LPR - 1)) == 0, "row lanes");
   static_assert(2 * (DK + DV) <= kCT, "one feature task per thread");
 
@@ -117,21 +121,15 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
 
   // ---- the state rows load behind the first windows
   const int row = tid / LPR;
-  const int col0 = (tid % LPR) * EPT;
+  const int col0 = (tid % LPR) * CPT;
   float* Sbh = p.S + (size_t(b) * Hv + h) * size_t(DV) * DK + size_t(row) * DK + col0;
   float srow[EPT];
-  if constexpr (EPT % 4 == 0) {
 #pragma unroll
-    for (int e = 0; e < EPT; e += 4) {
-      const float4 x = *reinterpret_cast<const float4*>(Sbh + e);
-      srow[e] = x.x;
-      srow[e + 1] = x.y;
-      srow[e + 2] = x.z;
-      srow[e + 3] = x.w;
-    }
-  } else {
+  for (int i = 0; i < R; ++i) {
+    float piece[CPT];
+    ld_slice<CPT>(Sbh + size_t(i) * RS * DK, piece);
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) srow[e] = Sbh[e];
+    for (int e = 0; e < CPT; ++e) srow[i * CPT + e] = piece[e];
   }
 
   // S_true = gamma * srow: one step costs one FMA for S.k and one for the
@@ -172,19 +170,28 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
     }
     __syncthreads();
     const int cnt = L - base < kMC ? L - base : kMC;
-    for (int mr = 0; mr < cnt; ++mr)
-      gamma = replay_step<EPT, LPR>(srow, &s_fk[mr][col0], s_fv[mr][row], s_al[base + mr], s_be[base + mr],
-                                    s_inv[mr], gamma);
+    for (int mr = 0; mr < cnt; ++mr) {
+      float kk[CPT], vr[R];
+      ld_slice<CPT>(&s_fk[mr][col0], kk);
+#pragma unroll
+      for (int i = 0; i < R; ++i) vr[i] = s_fv[mr][row + i * RS];
+      gamma = replay_rows<R, CPT, LPR>(srow, kk, vr, s_al[base + mr], s_be[base + mr], s_inv[mr], gamma);
+    }
     __syncthreads();  // chunk features consumed
   }
-  if constexpr (EPT % 4 == 0) {
 #pragma unroll
-    for (int e = 0; e < EPT; e += 4)
-      *reinterpret_cast<float4*>(Sbh + e) =
-          make_float4(srow[e] * gamma, srow[e + 1] * gamma, srow[e + 2] * gamma, srow[e + 3] * gamma);
-  } else {
+  for (int i = 0; i < R; ++i) {
+    float* dst = Sbh + size_t(i) * RS * DK;
+    if constexpr (CPT % 4 == 0) {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) Sbh[e] = srow[e] * gamma;
+      for (int e = 0; e < CPT; e += 4)
+        *reinterpret_cast<float4*>(dst + e) =
+            make_float4(srow[i * CPT + e] * gamma, srow[i * CPT + e + 1] * gamma, srow[i * CPT + e + 2] * gamma,
+                        srow[i * CPT + e + 3] * gamma);
+    } else {
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) dst[e] = srow[i * CPT + e] * gamma;
+    }
   }
 }
 

@@ -218,49 +218,62 @@ struct FeatWindow {
 };
 
 
-// One rank-1 step of the commit replay on a thread's EPT elements of a state
-// row (LPR lanes per row), Eq. 7 in the stored orientation:
-//   S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T.
-// The row is kept as S = gamma * stored (gamma: running product of alpha),
-// so a step is two FMAs per element; krow is the raw key, inv = 1 / ||k||
-// is folded into the scalars.  Returns the new gamma.
-template <int EPT, int LPR>
-__device__ __forceinline__ float replay_step(float (&sr)[EPT], const float* krow, float vr, float al, float be,
-                                             float inv, float gamma) {
-  float kk[EPT];
-  if constexpr (EPT % 4 == 0) {
+// One rank-1 step of the commit replay, Eq. 7 in the stored orientation,
+//   S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T,
+// on a thread's pieces of R state rows (CPT consecutive columns each, LPR
+// lanes per row; element i CPT + e is column e of piece i).  The rows are
+// kept as S = gamma * stored (gamma: running product of alpha), so a step is
+// two FMAs per element; kk is the thread's slice of the raw key, inv =
+// 1 / ||k|| is folded into the scalars and vr[i] is v of row piece i.  The
+// R rows share the key slice, which halves the LDS reads per element for
+// R = 2.  Returns the new gamma.
+template <int R, int CPT, int LPR>
+__device__ __forceinline__ float replay_rows(float (&sr)[R * CPT], const float (&kk)[CPT], const float (&vr)[R],
+                                            float al, float be, float inv, float gamma) {
+  float uu[R];
 #pragma unroll
-    for (int e = 0; e < EPT; e += 4) {
-      const float4 x = *reinterpret_cast<const float4*>(krow + e);
-      kk[e] = x.x;
-      kk[e + 1] = x.y;
-      kk[e + 2] = x.z;
-      kk[e + 3] = x.w;
-    }
-  } else {
+  for (int i = 0; i < R; ++i) {
+    float u[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) kk[e] = krow[e];
+    for (int e = 0; e < CPT; ++e) u[e & 3] += sr[i * CPT + e] * kk[e];
+    uu[i] = (u[0] + u[1]) + (u[2] + u[3]);
   }
-  float u0 = 0.0f, u1 = 0.0f;
 #pragma unroll
-  for (int e = 0; e + 1 < EPT; e += 2) {
-    u0 += sr[e] * kk[e];
-    u1 += sr[e + 1] * kk[e + 1];
-  }
-  if (EPT & 1) u0 += sr[EPT - 1] * kk[EPT - 1];
-  const float uu = group_sum<LPR>(u0 + u1) * inv;  // S_stored . k_hat
+  for (int i = 0; i < R; ++i) uu[i] = group_sum<LPR>(uu[i]) * inv;  // S_stored . k_hat
   // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
   // multiplied by 1 / ||k|| so that it applies to the raw key
   const float ag = al * gamma;
-  const float c = be * (vr - ag * uu) * __builtin_amdgcn_rcpf(ag) * inv;
+  const float ri = __builtin_amdgcn_rcpf(ag) * inv;
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) sr[e] += c * kk[e];
+  for (int i = 0; i < R; ++i) {
+    const float c = be * (vr[i] - ag * uu[i]) * ri;
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) sr[i * CPT + e] += c * kk[e];
+  }
   if (ag < 0x1p-60f) {  // keep the stored frame in range (uniform branch)
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) sr[e] *= ag;
+    for (int e = 0; e < R * CPT; ++e) sr[e] *= ag;
     return 1.0f;
   }
   return ag;
+}
+
+// CPT floats of an LDS row (16-byte pieces when CPT % 4 == 0)
+template <int CPT>
+__device__ __forceinline__ void ld_slice(const float* src, float (&x)[CPT]) {
+  if constexpr (CPT % 4 == 0) {
+#pragma unroll
+    for (int e = 0; e < CPT; e += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(src + e);
+      x[e] = v.x;
+      x[e + 1] = v.y;
+      x[e + 2] = v.z;
+      x[e + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) x[e] = src[e];
+  }
 }
 
 // ---------------------------------------------------------------------------

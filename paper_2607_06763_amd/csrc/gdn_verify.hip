@@ -345,68 +345,70 @@ struct HeadGates {
 };
 
 // Split of a DVS x DK state slice over the workgroup for the fused commit:
-// EPT consecutive elements of one row per thread, LPR lanes per row; the
-// first DVS * LPR threads own elements (all of them unless DVS DK < kVT).
+// each thread holds R rows (q + i RS, i < R, RS = DVS / R) times CPT
+// consecutive columns; LPR lanes share a row.  Two rows per thread halve the
+// LDS reads of the key slices in the replay (every row of a step reads the
+// same key).  The first DVS DK / EPT threads own elements (all of them
+// unless DVS DK < kVT).  Element e of a thread is row row(tid, e / CPT),
+// column col0(tid) + e % CPT.
 template <int DK, int DVS>
 struct FusedSplit {
   static constexpr int EPT = DVS * DK >= kVT ? DVS * DK / kVT : 1;
-  static constexpr int LPR = DK / EPT;
-  static_assert(EPT >= 1 && LPR >= 1 && LPR <= 64 && (LPR & (LPR - 1)) == 0, "fused state split");
-  __device__ static __forceinline__ bool owns(int tid) { return tid < DVS * LPR; }
-  __device__ static __forceinline__ int row(int tid) { return owns(tid) ? tid / LPR : DVS - 1; }
-  __device__ static __forceinline__ int col0(int tid) { return (tid % LPR) * EPT; }
-  __device__ static __forceinline__ void load(const float* src, float (&x)[EPT]) {
-    if constexpr (EPT % 4 == 0) {
-#pragma unroll
-      for (int e = 0; e < EPT; e += 4) {
-        const float4 v = *reinterpret_cast<const float4*>(src + e);
-        x[e] = v.x;
-        x[e + 1] = v.y;
-        x[e + 2] = v.z;
-        x[e + 3] = v.w;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) x[e] = src[e];
-    }
-  }
-  __device__ static __forceinline__ void store(float* dst, const float (&x)[EPT]) {
-    if constexpr (EPT % 4 == 0) {
-#pragma unroll
-      for (int e = 0; e < EPT; e += 4)
-        *reinterpret_cast<float4*>(dst + e) = make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) dst[e] = x[e];
-    }
-  }
+  static constexpr int R = EPT >= 16 ? 2 : 1;
+  static constexpr int CPT = EPT / R;
+  static constexpr int LPR = DK / CPT;
+  static constexpr int RS = DVS / R;
+  static_assert(CPT >= 1 && LPR >= 1 && LPR <= 64 && (LPR & (LPR - 1)) == 0 && DVS % R == 0, "fused state split");
+  __device__ static __forceinline__ bool owns(int tid) { return tid < RS * LPR; }
+  __device__ static __forceinline__ int row(int tid, int i) { return (owns(tid) ? tid / LPR : RS - 1) + i * RS; }
+  __device__ static __forceinline__ int col0(int tid) { return (tid % LPR) * CPT; }
 };
 
 // State rows c0 .. c0 + DVS of head h (before the fused commit) in the
-// commit layout.  Threads that own no elements load row 0 (never stored).
+// commit layout.  Threads that own no elements load rows of thread 0 (never
+// stored).
 template <int DK, int DVS>
 __device__ __forceinline__ void load_state_rows(const float* S, int b, int Hv, int DV, int h, int c0, int tid,
                                                 float (&sr)[FusedSplit<DK, DVS>::EPT]) {
   using FS = FusedSplit<DK, DVS>;
   const int t = FS::owns(tid) ? tid : 0;
-  FS::load(S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(t)) * DK + FS::col0(t), sr);
+#pragma unroll
+  for (int i = 0; i < FS::R; ++i) {
+    const float* src = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(t, i)) * DK + FS::col0(t);
+    if constexpr (FS::CPT % 4 == 0) {
+#pragma unroll
+      for (int e = 0; e < FS::CPT; e += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(src + e);
+        sr[i * FS::CPT + e] = v.x;
+        sr[i * FS::CPT + e + 1] = v.y;
+        sr[i * FS::CPT + e + 2] = v.z;
+        sr[i * FS::CPT + e + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < FS::CPT; ++e) sr[i * FS::CPT + e] = src[e];
+    }
+  }
 }
 
-// Stores float4 groups [j0, j1) of this thread's state elements to the rows
-// of head h (all elements when EPT is not a multiple of 4 and j0 == 0).
+// Stores this thread's state elements to the rows of head h.
 template <int DK, int DVS>
 __device__ __forceinline__ void store_state_rows(float* S, int b, int Hv, int DV, int h, int c0, int tid,
-                                                 const float (&sr)[FusedSplit<DK, DVS>::EPT], int j0, int j1) {
+                                                 const float (&sr)[FusedSplit<DK, DVS>::EPT]) {
   using FS = FusedSplit<DK, DVS>;
   if (!FS::owns(tid)) return;
-  float* dst = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(tid)) * DK + FS::col0(tid);
-  if constexpr (FS::EPT % 4 == 0) {
 #pragma unroll
-    for (int j = 0; j < FS::EPT / 4; ++j)
-      if (j >= j0 && j < j1)
-        *reinterpret_cast<float4*>(dst + 4 * j) = make_float4(sr[4 * j], sr[4 * j + 1], sr[4 * j + 2], sr[4 * j + 3]);
-  } else {
-    if (j0 == 0) FS::store(dst, sr);
+  for (int i = 0; i < FS::R; ++i) {
+    float* dst = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(tid, i)) * DK + FS::col0(tid);
+    if constexpr (FS::CPT % 4 == 0) {
+#pragma unroll
+      for (int e = 0; e < FS::CPT; e += 4)
+        *reinterpret_cast<float4*>(dst + e) = make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1],
+                                                          sr[i * FS::CPT + e + 2], sr[i * FS::CPT + e + 3]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < FS::CPT; ++e) dst[e] = sr[i * FS::CPT + e];
+    }
   }
 }
 
@@ -414,7 +416,7 @@ __device__ __forceinline__ void store_state_rows(float* S, int b, int Hv, int DV
 // s_ppath) into the state rows c0 .. c0 + DVS of value head h: features of
 // the path (previous step's raw inputs, conv state before the commit), then
 // one rank-1 step per path node on this thread's elements of the rows
-// (Eq. 7, see replay_step).  sr holds the elements before the commit on
+// (Eq. 7, see replay_rows).  sr holds the elements before the commit on
 // entry (load_state_rows) and after it on return; the caller stores them
 // (store_state_rows).  Uses lds (the value-tile region) and ends with a
 // barrier; a uniform no-op when L = 0.
@@ -423,7 +425,7 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
                                              int b, int g, int h, int c0, int tid,
                                              float (&sr)[FusedSplit<DK, DVS>::EPT]) {
   using FS = FusedSplit<DK, DVS>;
-  constexpr int EPT = FS::EPT, LPR = FS::LPR;
+  constexpr int EPT = FS::EPT, LPR = FS::LPR, R = FS::R, CPT = FS::CPT;
   constexpr int FP = 4 * (DK + DVS) <= kVT ? 4 : 2;  // feature parts per chunk
   constexpr int FN = kMC / FP;                       // path nodes per feature task
   static_assert(FP * (DK + DVS) <= kVT, "one feature task per thread");
@@ -452,7 +454,7 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
                           : static_cast<const TIn*>(p.pk) + size_t(b) * T * Hk * DK + size_t(g) * DK + fc;
   const size_t fstride = vtask ? size_t(Hv) * DV : size_t(Hk) * DK;
   const float* fcs = p.conv_state + size_t(b) * 3 * C + fch;
-  const int row = FS::row(tid), col0 = FS::col0(tid);
+  const int row0 = FS::row(tid, 0), col0 = FS::col0(tid);
   float gamma = 1.0f;
   for (int base = 0; base < L; base += kMC) {
     FeatWindow<TIn, FN> win;
@@ -491,9 +493,13 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
     }
     __syncthreads();
     const int cnt = L - base < kMC ? L - base : kMC;
-    for (int mr = 0; mr < cnt; ++mr)
-      gamma = replay_step<EPT, LPR>(sr, s_fk + mr * DK + col0, s_fv[mr * DVS + row], s_al[base + mr],
-                                    s_be[base + mr], s_inv[mr], gamma);
+    for (int mr = 0; mr < cnt; ++mr) {
+      float kk[CPT], vr[R];
+      ld_slice<CPT>(s_fk + mr * DK + col0, kk);
+#pragma unroll
+      for (int i = 0; i < R; ++i) vr[i] = s_fv[mr * DVS + row0 + i * FS::RS];
+      gamma = replay_rows<R, CPT, LPR>(sr, kk, vr, s_al[base + mr], s_be[base + mr], s_inv[mr], gamma);
+    }
     __syncthreads();  // chunk features consumed
   }
 #pragma unroll
@@ -638,7 +644,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       for (int hh = 0; hh < p.hpw; ++hh) {
         load_state_rows<DK, DVS>(p.S, b, Hv, DV, h0 + hh, c0, tid, sr);
         fused_commit<DK, DVS, TIn>(p, s_rv, s_ppath, Lp, b, g, h0 + hh, c0, tid, sr);
-        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h0 + hh, c0, tid, sr, 0, NSR);
+        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h0 + hh, c0, tid, sr);
       }
       fused_conv_out<DK, DVS, TIn>(p, s_ppath, Lp, b, g, h0, c0, blockIdx.x == 0 && blockIdx.y % nhg == 0, tid);
     }
@@ -834,7 +840,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       int trow[2][4];  // recomputed per head: fewer registers held across heads
       conv_rows(s_dep, s_ppos, T, pos, act, trow);
       if constexpr (FUSED)
-        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h, c0, tid, sr, 0, NSR);
+        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h, c0, tid, sr);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -986,23 +992,29 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       _Float16* s_h = reinterpret_cast<_Float16*>(s_rv);
       if constexpr (FUSED) {
         using FS = FusedSplit<DK, DVS>;
-        float m = 0.0f;
 #pragma unroll
-        for (int e = 0; e < NSR; ++e) m = fmaxf(m, fabsf(sr[e]));
-        m = group_max<FS::LPR>(m);
-        float sc, inv;
-        row_scale(m, sc, inv);
-        if (FS::owns(tid)) {
-          const int off = FS::row(tid) * (KAPPA + kSPad) + FS::col0(tid);
-          if constexpr (NSR % 4 == 0) {
+        for (int i = 0; i < FS::R; ++i) {
+          float m = 0.0f;
 #pragma unroll
-            for (int e = 0; e < NSR; e += 4)
-              *reinterpret_cast<uint2*>(s_h + off + e) = to_f16x4(make_float4(sr[e], sr[e + 1], sr[e + 2], sr[e + 3]), sc);
-          } else {
+          for (int e = 0; e < FS::CPT; ++e) m = fmaxf(m, fabsf(sr[i * FS::CPT + e]));
+          m = group_max<FS::LPR>(m);
+          float sc, inv;
+          row_scale(m, sc, inv);
+          if (FS::owns(tid)) {
+            const int off = FS::row(tid, i) * (KAPPA + kSPad) + FS::col0(tid);
+            if constexpr (FS::CPT % 4 == 0) {
 #pragma unroll
-            for (int e = 0; e < NSR; ++e) s_h[off + e] = (_Float16)(sr[e] * sc);
+              for (int e = 0; e < FS::CPT; e += 4)
+                *reinterpret_cast<uint2*>(s_h + off + e) =
+                    to_f16x4(make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1], sr[i * FS::CPT + e + 2],
+                                         sr[i * FS::CPT + e + 3]),
+                             sc);
+            } else {
+#pragma unroll
+              for (int e = 0; e < FS::CPT; ++e) s_h[off + e] = (_Float16)(sr[i * FS::CPT + e] * sc);
+            }
+            if (FS::col0(tid) == 0) s_rs[FS::row(tid, i)] = inv;
           }
-          if (FS::col0(tid) == 0) s_rs[FS::row(tid)] = inv;
         }
       } else {
 #pragma unroll
