@@ -365,50 +365,60 @@ struct FusedSplit {
 };
 
 // State rows c0 .. c0 + DVS of head h (before the fused commit) in the
-// commit layout.  Threads that own no elements load rows of thread 0 (never
-// stored).
-template <int DK, int DVS>
+// commit layout, part `part` of PARTS: the 16-byte groups g (4 consecutive
+// elements of one row piece) with g % PARTS == part, or all elements when a
+// row piece is not a multiple of 4 wide (part 0 only).  Loading a state in
+// parts lets the loads ride along with the compute phases instead of
+// stalling the issuing wave as one burst.  Threads that own no elements load
+// rows of thread 0 (never stored).
+template <int DK, int DVS, int PARTS = 1>
 __device__ __forceinline__ void load_state_rows(const float* S, int b, int Hv, int DV, int h, int c0, int tid,
-                                                float (&sr)[FusedSplit<DK, DVS>::EPT]) {
+                                                float (&sr)[FusedSplit<DK, DVS>::EPT], int part = 0) {
   using FS = FusedSplit<DK, DVS>;
   const int t = FS::owns(tid) ? tid : 0;
+  const float* base = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(t, 0)) * DK + FS::col0(t);
+  if constexpr (FS::CPT % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < FS::R; ++i) {
-    const float* src = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(t, i)) * DK + FS::col0(t);
-    if constexpr (FS::CPT % 4 == 0) {
-#pragma unroll
-      for (int e = 0; e < FS::CPT; e += 4) {
-        const float4 v = *reinterpret_cast<const float4*>(src + e);
-        sr[i * FS::CPT + e] = v.x;
-        sr[i * FS::CPT + e + 1] = v.y;
-        sr[i * FS::CPT + e + 2] = v.z;
-        sr[i * FS::CPT + e + 3] = v.w;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < FS::CPT; ++e) sr[i * FS::CPT + e] = src[e];
+    for (int gi = 0; gi < FS::EPT / 4; ++gi) {
+      if (gi % PARTS != part) continue;
+      const int i = gi / (FS::CPT / 4), e = 4 * (gi % (FS::CPT / 4));
+      const float4 v = *reinterpret_cast<const float4*>(base + size_t(i) * FS::RS * DK + e);
+      sr[i * FS::CPT + e] = v.x;
+      sr[i * FS::CPT + e + 1] = v.y;
+      sr[i * FS::CPT + e + 2] = v.z;
+      sr[i * FS::CPT + e + 3] = v.w;
     }
+  } else {
+    if (part != 0) return;
+#pragma unroll
+    for (int i = 0; i < FS::R; ++i)
+#pragma unroll
+      for (int e = 0; e < FS::CPT; ++e) sr[i * FS::CPT + e] = base[size_t(i) * FS::RS * DK + e];
   }
 }
 
-// Stores this thread's state elements to the rows of head h.
-template <int DK, int DVS>
+// Stores part `part` of PARTS of this thread's state elements to the rows of
+// head h (the grouping of load_state_rows).
+template <int DK, int DVS, int PARTS = 1>
 __device__ __forceinline__ void store_state_rows(float* S, int b, int Hv, int DV, int h, int c0, int tid,
-                                                 const float (&sr)[FusedSplit<DK, DVS>::EPT]) {
+                                                 const float (&sr)[FusedSplit<DK, DVS>::EPT], int part = 0) {
   using FS = FusedSplit<DK, DVS>;
   if (!FS::owns(tid)) return;
+  float* base = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(tid, 0)) * DK + FS::col0(tid);
+  if constexpr (FS::CPT % 4 == 0) {
 #pragma unroll
-  for (int i = 0; i < FS::R; ++i) {
-    float* dst = S + ((size_t(b) * Hv + h) * DV + c0 + FS::row(tid, i)) * DK + FS::col0(tid);
-    if constexpr (FS::CPT % 4 == 0) {
-#pragma unroll
-      for (int e = 0; e < FS::CPT; e += 4)
-        *reinterpret_cast<float4*>(dst + e) = make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1],
-                                                          sr[i * FS::CPT + e + 2], sr[i * FS::CPT + e + 3]);
-    } else {
-#pragma unroll
-      for (int e = 0; e < FS::CPT; ++e) dst[e] = sr[i * FS::CPT + e];
+    for (int gi = 0; gi < FS::EPT / 4; ++gi) {
+      if (gi % PARTS != part) continue;
+      const int i = gi / (FS::CPT / 4), e = 4 * (gi % (FS::CPT / 4));
+      *reinterpret_cast<float4*>(base + size_t(i) * FS::RS * DK + e) =
+          make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1], sr[i * FS::CPT + e + 2], sr[i * FS::CPT + e + 3]);
     }
+  } else {
+    if (part != 0) return;
+#pragma unroll
+    for (int i = 0; i < FS::R; ++i)
+#pragma unroll
+      for (int e = 0; e < FS::CPT; ++e) base[size_t(i) * FS::RS * DK + e] = sr[i * FS::CPT + e];
   }
 }
 
@@ -833,6 +843,11 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
     }
     gpf.store(s_al, s_be, s_wv, s_v, VROW, T, tid);
+    // fused step: the committed rows of this head go to S in four parts
+    // spread over 2a .. 2c, behind compute
+    constexpr int kSP = 4;
+    if constexpr (FUSED)
+      if (Lp > 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 0);
     __syncthreads();
     // 2b: v~ of this lane's two nodes, channels lane_chan(lo, r, vsw)
     float vt[2][VPL];
@@ -840,7 +855,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       int trow[2][4];  // recomputed per head: fewer registers held across heads
       conv_rows(s_dep, s_ppos, T, pos, act, trow);
       if constexpr (FUSED)
-        if (Lp > 0) store_state_rows<DK, DVS>(p.S, b, Hv, DV, h, c0, tid, sr);
+        if (Lp > 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 1);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -912,6 +927,8 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
 #pragma unroll
       for (int c = 0; c < KPL; ++c) x[u][c] *= r;
+      if constexpr (FUSED)
+        if (Lp > 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 2 + u);
     }
     // a_i x~_i and the value accumulators move to the MFMA layout:
     //   X~^T B operand, k block kb: lane (l16, mlg) holds channels 32 kb + 8 mlg + e
