@@ -365,12 +365,12 @@ struct FusedSplit {
 };
 
 // State rows c0 .. c0 + DVS of head h (before the fused commit) in the
-// commit layout, part `part` of PARTS: the 16-byte groups g (4 consecutive
-// elements of one row piece) with g % PARTS == part, or all elements when a
-// row piece is not a multiple of 4 wide (part 0 only).  Loading a state in
-// parts lets the loads ride along with the compute phases instead of
-// stalling the issuing wave as one burst.  Threads that own no elements load
-// rows of thread 0 (never stored).
+// commit layout, part `part` of PARTS: the run of 16-byte groups (4
+// consecutive elements of one row piece) [part G / PARTS, (part + 1) G /
+// PARTS) of the thread's G groups, or all elements when a row piece is not a
+// multiple of 4 wide (part 0 only).  With PARTS <= R a part is whole row
+// pieces, so the threads of a row still cover whole cache lines.  Threads
+// that own no elements load rows of thread 0 (never stored).
 template <int DK, int DVS, int PARTS = 1>
 __device__ __forceinline__ void load_state_rows(const float* S, int b, int Hv, int DV, int h, int c0, int tid,
                                                 float (&sr)[FusedSplit<DK, DVS>::EPT], int part = 0) {
@@ -380,7 +380,7 @@ __device__ __forceinline__ void load_state_rows(const float* S, int b, int Hv, i
   if constexpr (FS::CPT % 4 == 0) {
 #pragma unroll
     for (int gi = 0; gi < FS::EPT / 4; ++gi) {
-      if (gi % PARTS != part) continue;
+      if (gi * PARTS / (FS::EPT / 4) != part) continue;
       const int i = gi / (FS::CPT / 4), e = 4 * (gi % (FS::CPT / 4));
       const float4 v = *reinterpret_cast<const float4*>(base + size_t(i) * FS::RS * DK + e);
       sr[i * FS::CPT + e] = v.x;
@@ -408,7 +408,7 @@ __device__ __forceinline__ void store_state_rows(float* S, int b, int Hv, int DV
   if constexpr (FS::CPT % 4 == 0) {
 #pragma unroll
     for (int gi = 0; gi < FS::EPT / 4; ++gi) {
-      if (gi % PARTS != part) continue;
+      if (gi * PARTS / (FS::EPT / 4) != part) continue;
       const int i = gi / (FS::CPT / 4), e = 4 * (gi % (FS::CPT / 4));
       *reinterpret_cast<float4*>(base + size_t(i) * FS::RS * DK + e) =
           make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1], sr[i * FS::CPT + e + 2], sr[i * FS::CPT + e + 3]);
@@ -843,9 +843,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
     }
     gpf.store(s_al, s_be, s_wv, s_v, VROW, T, tid);
-    // fused step: the committed rows of this head go to S in four parts
-    // spread over 2a .. 2c, behind compute
-    constexpr int kSP = 4;
+    // fused step: the committed rows of this head go to S in two parts (one
+    // row piece each, whole cache lines) spread over 2a .. 2c, behind compute
+    constexpr int kSP = 2;
     if constexpr (FUSED)
       if (Lp > 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 0);
     __syncthreads();
@@ -854,8 +854,6 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     {
       int trow[2][4];  // recomputed per head: fewer registers held across heads
       conv_rows(s_dep, s_ppos, T, pos, act, trow);
-      if constexpr (FUSED)
-        if (Lp > 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 1);
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -928,7 +926,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
 #pragma unroll
       for (int c = 0; c < KPL; ++c) x[u][c] *= r;
       if constexpr (FUSED)
-        if (Lp > 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 2 + u);
+        if (Lp > 0 && u == 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 1);
     }
     // a_i x~_i and the value accumulators move to the MFMA layout:
     //   X~^T B operand, k block kb: lane (l16, mlg) holds channels 32 kb + 8 mlg + e
