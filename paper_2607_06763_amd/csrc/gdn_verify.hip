@@ -923,35 +923,75 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         r *= al;
         t = nx;
       }
+      // a_i x~ rounded to fp32 first in both kernels (no fused multiply +
+      // fp16 conversion), so that they round the B operand identically
 #pragma unroll
-      for (int c = 0; c < KPL; ++c) x[u][c] *= r;
+      for (int c = 0; c < KPL; ++c) {
+        x[u][c] *= r;
+        pin(x[u][c]);
+      }
       if constexpr (FUSED)
         if (Lp > 0 && u == 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 1);
     }
     // a_i x~_i and the value accumulators move to the MFMA layout:
     //   X~^T B operand, k block kb: lane (l16, mlg) holds channels 32 kb + 8 mlg + e
     //   O^T accumulator, tile n:    lane (l16, mlg) holds channels 16 n + 4 mlg + e
-    float xm[KB][8];
+    // x~ goes over as fp16 (the B operand's type, |x~| <= |q~| = 1).  In the
+    // verify kernel both nodes of a lane share one dword (node 0 low half),
+    // so one ds_bpermute per channel serves the columns of both halves; the
+    // fused step, whose state rows occupy 32 more registers here, moves them
+    // one node at a time (the packed form would spill there)
+    f16x8 xb[KB];  // B operand of X~^T
+    if constexpr (!FUSED) {
+      uint32_t px[KPL];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
+      for (int rr = 0; rr < KPL; ++rr)
+        px[rr] = uint32_t(__builtin_bit_cast(uint16_t, (_Float16)x[0][rr])) |
+                 (uint32_t(__builtin_bit_cast(uint16_t, (_Float16)x[1][rr])) << 16);
+      __builtin_amdgcn_sched_barrier(0);  // x~ in fp32 is dead from here on
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        int rr, src;
-        bool valid = true;
-        if constexpr (DK >= 32) {
-          rr = 4 * kb + (e & 3);
-          src = sbase + 2 * mlg + (e >> 2);
-        } else {
-          rr = e & 1;
-          src = (sbase + 4 * mlg + (e >> 1)) & 63;
-          valid = mlg < 2;
+      for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          int rr, src;
+          bool valid = true;
+          if constexpr (DK >= 32) {
+            rr = 4 * kb + (e & 3);
+            src = sbase + 2 * mlg + (e >> 2);
+          } else {
+            rr = e & 1;
+            src = (sbase + 4 * mlg + (e >> 1)) & 63;
+            valid = mlg < 2;
+          }
+          const uint32_t w = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(px[rr])));
+          const uint16_t hb = uint16_t(mhalf ? (w >> 16) : (w & 0xffffu));
+          xb[kb][e] = valid ? __builtin_bit_cast(_Float16, hb) : (_Float16)0.0f;
         }
-        const float a0 = lane_gather(x[0][rr], src);
-        const float a1 = lane_gather(x[1][rr], src);
-        xm[kb][e] = valid ? (mhalf ? a1 : a0) : 0.0f;
-        pin(xm[kb][e]);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      __builtin_amdgcn_sched_barrier(0);
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          int rr, src;
+          bool valid = true;
+          if constexpr (DK >= 32) {
+            rr = 4 * kb + (e & 3);
+            src = sbase + 2 * mlg + (e >> 2);
+          } else {
+            rr = e & 1;
+            src = (sbase + 4 * mlg + (e >> 1)) & 63;
+            valid = mlg < 2;
+          }
+          const float a0 = lane_gather(x[0][rr], src);
+          const float a1 = lane_gather(x[1][rr], src);
+          float xv = valid ? (mhalf ? a1 : a0) : 0.0f;
+          pin(xv);
+          xb[kb][e] = (_Float16)xv;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     float am[NT][4];
 #pragma unroll
@@ -978,13 +1018,11 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     if (l16 & 1) {
       if constexpr (DK >= 64) {
 #pragma unroll
-        for (int kb = 0; kb < KB; kb += 2)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float t0 = xm[kb][e];
-            xm[kb][e] = xm[kb + 1][e];
-            xm[kb + 1][e] = t0;
-          }
+        for (int kb = 0; kb < KB; kb += 2) {
+          const f16x8 t0 = xb[kb];
+          xb[kb] = xb[kb + 1];
+          xb[kb + 1] = t0;
+        }
       }
       if constexpr (DVS >= 64) {
 #pragma unroll
@@ -1065,11 +1103,6 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     // 2e: P^T = (D S0) X~^T on MFMA (fp16 operands, fp32 accumulation);
     //     O^T = scale (D^-1 P^T + ACC^T) in the accumulator layout; store
     {
-      f16x8 xb[KB];
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) xb[kb][e] = (_Float16)xm[kb][e];
       const _Float16* s_h = reinterpret_cast<const _Float16*>(s_rv);
       const int node = mpos < T ? s_ord[mpos] : 0;
       float* orow_p = p.out + (size_t(b) * T + node) * orow + size_t(h) * DV + c0;
