@@ -994,24 +994,49 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
     }
     float am[NT][4];
+    if constexpr (DVS >= 32) {
+      // Tile n reads the lanes o = 4 (n & 1) + mlg of a group.  First the
+      // halves of each group trade registers (lane o <-> 7 - o, one DPP move
+      // per register): lanes 0..3 then hold node 0's channels of both tile
+      // parities (acc[0]: own, acc[1]: from lane 7 - o), lanes 4..7 node 1's
+      // (acc[0]: from lane 7 - o, acc[1]: own), so that every ds_bpermute
+      // moves a value its destination column needs: 32 instead of 64.
+      const bool lowh = lo < 4;
 #pragma unroll
-    for (int n = 0; n < NT; ++n) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        int rr, src;
-        if constexpr (DVS >= 32) {
-          rr = 4 * (n >> 1) + e;
-          src = sbase + 4 * (n & 1) + mlg;
-        } else {
-          rr = e & 1;
-          src = sbase + 2 * mlg + (e >> 1);
-        }
-        const float a0 = lane_gather(acc[0][rr], src);
-        const float a1 = lane_gather(acc[1][rr], src);
-        am[n][e] = mhalf ? a1 : a0;
-        pin(am[n][e]);
+      for (int rr = 0; rr < VPL; ++rr) {
+        const float send = lowh ? acc[1][rr] : acc[0][rr];
+        const float recv = dpp_f<kDppRowHalfMirror>(send);
+        const float b0 = lowh ? acc[0][rr] : recv;
+        const float b1 = lowh ? recv : acc[1][rr];
+        acc[0][rr] = b0;
+        acc[1][rr] = b1;
       }
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int rr = 4 * (n >> 1) + e;
+          // source lane of (node half, tile parity): own data at mlg / 4 + mlg,
+          // traded data at the mirror lane 3 - mlg / 7 - mlg
+          const int sl = (n & 1) ? (mhalf ? 4 + mlg : 3 - mlg) : (mhalf ? 7 - mlg : mlg);
+          am[n][e] = lane_gather((n & 1) ? acc[1][rr] : acc[0][rr], sbase + sl);
+          pin(am[n][e]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int rr = e & 1, src = sbase + 2 * mlg + (e >> 1);
+          const float a0 = lane_gather(acc[0][rr], src);
+          const float a1 = lane_gather(acc[1][rr], src);
+          am[n][e] = mhalf ? a1 : a0;
+          pin(am[n][e]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
     // a column whose source lane group is odd (l16 odd) received the 32-channel
     // chunks in the swapped order c ^ 1: put them back in place
