@@ -936,61 +936,49 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     // a_i x~_i and the value accumulators move to the MFMA layout:
     //   X~^T B operand, k block kb: lane (l16, mlg) holds channels 32 kb + 8 mlg + e
     //   O^T accumulator, tile n:    lane (l16, mlg) holds channels 16 n + 4 mlg + e
-    // x~ goes over as fp16 (the B operand's type, |x~| <= |q~| = 1).  In the
-    // verify kernel both nodes of a lane share one dword (node 0 low half),
-    // so one ds_bpermute per channel serves the columns of both halves; the
-    // fused step, whose state rows occupy 32 more registers here, moves them
-    // one node at a time (the packed form would spill there)
+    // x~ goes over as fp16 (the B operand's type, |x~| <= |q~| = 1).  Key
+    // block kb of column (node, mlg) reads lanes 2 mlg (e < 4) and 2 mlg + 1
+    // (e >= 4) of the node's group.  The even and odd lanes of a group first
+    // trade registers by DPP (lane o <-> o ^ 1): even lanes then hold node 0's
+    // channels of both lanes, odd lanes node 1's, packed as fp16 pairs (even
+    // lane's channel low), so one ds_bpermute moves two needed values: 16 per
+    // lane instead of 64.
     f16x8 xb[KB];  // B operand of X~^T
-    if constexpr (!FUSED) {
+    if constexpr (DK >= 32) {
+      const bool evn = (lo & 1) == 0;
       uint32_t px[KPL];
 #pragma unroll
-      for (int rr = 0; rr < KPL; ++rr)
-        px[rr] = uint32_t(__builtin_bit_cast(uint16_t, (_Float16)x[0][rr])) |
-                 (uint32_t(__builtin_bit_cast(uint16_t, (_Float16)x[1][rr])) << 16);
+      for (int rr = 0; rr < KPL; ++rr) {
+        const float send = evn ? x[1][rr] : x[0][rr];
+        const float recv = dpp_f<kDppQuadXor1>(send);
+        const float b0 = evn ? x[0][rr] : recv;
+        const float b1 = evn ? recv : x[1][rr];
+        px[rr] = uint32_t(__builtin_bit_cast(uint16_t, (_Float16)b0)) |
+                 (uint32_t(__builtin_bit_cast(uint16_t, (_Float16)b1)) << 16);
+      }
       __builtin_amdgcn_sched_barrier(0);  // x~ in fp32 is dead from here on
+      const int src = sbase + 2 * mlg + mhalf;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          int rr, src;
-          bool valid = true;
-          if constexpr (DK >= 32) {
-            rr = 4 * kb + (e & 3);
-            src = sbase + 2 * mlg + (e >> 2);
-          } else {
-            rr = e & 1;
-            src = (sbase + 4 * mlg + (e >> 1)) & 63;
-            valid = mlg < 2;
-          }
-          const uint32_t w = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(px[rr])));
-          const uint16_t hb = uint16_t(mhalf ? (w >> 16) : (w & 0xffffu));
-          xb[kb][e] = valid ? __builtin_bit_cast(_Float16, hb) : (_Float16)0.0f;
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t w = uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(px[4 * kb + q])));
+          xb[kb][q] = __builtin_bit_cast(_Float16, uint16_t(w & 0xffffu));
+          xb[kb][q + 4] = __builtin_bit_cast(_Float16, uint16_t(w >> 16));
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
     } else {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          int rr, src;
-          bool valid = true;
-          if constexpr (DK >= 32) {
-            rr = 4 * kb + (e & 3);
-            src = sbase + 2 * mlg + (e >> 2);
-          } else {
-            rr = e & 1;
-            src = (sbase + 4 * mlg + (e >> 1)) & 63;
-            valid = mlg < 2;
-          }
+          const int rr = e & 1, src = (sbase + 4 * mlg + (e >> 1)) & 63;
           const float a0 = lane_gather(x[0][rr], src);
           const float a1 = lane_gather(x[1][rr], src);
-          float xv = valid ? (mhalf ? a1 : a0) : 0.0f;
+          float xv = mlg < 2 ? (mhalf ? a1 : a0) : 0.0f;
           pin(xv);
           xb[kb][e] = (_Float16)xv;
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
     float am[NT][4];
