@@ -249,14 +249,32 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
 // Only the loads j with j % PARTS == part are issued, so that a prefetch can
 // be spread over the steps of a compute phase (a burst of loads holds the
 // issuing wave until most of its data has arrived).
+// When the slice has at least one float4 per thread, each thread takes NS0
+// consecutive float4 of one row (S0 rows of TPR threads), so that a row's
+// scale needs one max over TPR lanes; otherwise thread tid takes float4
+// j kVT + tid.
+template <int DK, int DVS>
+struct S0Split {
+  static constexpr int N4 = DVS * DK / 4;        // float4 of the slice
+  static constexpr bool kRows = N4 >= kVT;       // the row-wise split applies
+  static constexpr int NS0 = kRows ? N4 / kVT : 1;
+  static constexpr int TPR = kRows ? DK / 4 / NS0 : 1;  // threads per row
+  static_assert(!kRows || (TPR >= 1 && TPR <= 32 && NS0 * TPR == DK / 4), "S0 split");
+};
 template <int DK, int DVS, int NS0, int PARTS = 1>
 __device__ __forceinline__ void prefetch_s0(const float* S0bh, int tid, float4 (&pf)[NS0], int part = 0) {
-  constexpr int n4 = DVS * DK / 4;
+  using SP = S0Split<DK, DVS>;
+  static_assert(SP::NS0 == NS0, "S0 split");
 #pragma unroll
   for (int j = 0; j < NS0; ++j) {
     if (j % PARTS != part) continue;
-    const int idx = j * kVT + tid;
-    pf[j] = idx < n4 ? reinterpret_cast<const float4*>(S0bh)[idx] : make_float4(0.f, 0.f, 0.f, 0.f);
+    if constexpr (SP::kRows) {
+      const int idx = (tid / SP::TPR) * (DK / 4) + (tid % SP::TPR) * NS0 + j;
+      pf[j] = reinterpret_cast<const float4*>(S0bh)[idx];
+    } else {
+      const int idx = j * kVT + tid;
+      pf[j] = idx < SP::N4 ? reinterpret_cast<const float4*>(S0bh)[idx] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   }
 }
 
@@ -574,7 +592,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   constexpr int NT = DVS / 16;                // 16-row value tiles of this slice
   constexpr int VROW = row_floats<DVS>();     // v~ / staging row stride (floats)
   constexpr int EPC = 16 / sizeof(TIn);
-  constexpr int NS0 = FUSED ? 1 : (DVS * DK / 4 + kVT - 1) / kVT;  // S0 float4 per thread
+  constexpr int NS0 = FUSED ? 1 : S0Split<DK, DVS>::NS0;  // S0 float4 per thread
   constexpr int NSR = FUSED ? FusedSplit<DK, DVS>::EPT : 1;       // state floats per thread (fused)
   constexpr int NVC = (kVMaxT * DVS / EPC + kVT - 1) / kVT;  // raw-v chunks per thread
   constexpr int QCPR = DK / EPC;                             // raw q/k chunks per row
@@ -1082,6 +1100,23 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
             if (FS::col0(tid) == 0) s_rs[FS::row(tid, i)] = inv;
           }
         }
+      } else if constexpr (S0Split<DK, DVS>::kRows) {
+        // NS0 float4 of row tid / TPR: one scale per row from a TPR-lane max
+        using SP = S0Split<DK, DVS>;
+        float m = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NS0; ++j) {
+          const float4 x = s0pf[j];
+          m = fmaxf(m, fmaxf(fmaxf(fabsf(x.x), fabsf(x.y)), fmaxf(fabsf(x.z), fabsf(x.w))));
+        }
+        m = group_max<SP::TPR>(m);
+        float sc, inv;
+        row_scale(m, sc, inv);
+        const int row = tid / SP::TPR, k0 = (tid % SP::TPR) * NS0;
+#pragma unroll
+        for (int j = 0; j < NS0; ++j)
+          *reinterpret_cast<uint2*>(s_h + row * (KAPPA + kSPad) + 4 * (k0 + j)) = to_f16x4(s0pf[j], sc);
+        if (k0 == 0) s_rs[row] = inv;
       } else {
 #pragma unroll
         for (int j = 0; j < NS0; ++j) {
