@@ -220,9 +220,9 @@ __device__ __forceinline__ uint2 to_f16x4(float4 x, float sc) {
 
 // LDS regions (bytes) for a tree of T slots, key dim DK and value slice DVS
 struct VerifySmem {
-  size_t rk, rv, meta, total;
+  size_t rk, rv, meta, p0, total;
 };
-__host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
+__host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS, bool fused) {
   const int TP = (T + 15) & ~15;
   const int kappa = DK >= 32 ? DK : 32;
   const size_t rows = size_t(TP > T + 3 ? TP : T + 3);
@@ -241,7 +241,12 @@ __host__ __device__ inline VerifySmem verify_smem(int T, int DK, int DVS) {
            + size_t(8 * DK) * 4 + size_t(4 * DVS) * 4       // q/k and v conv weights
            + size_t(kVMaxT) * 4                             // previous path (fused step)
            + size_t(kVMaxT) * 4;                            // S0 row scales
-  s.total = s.rk + s.rv + s.meta;
+  // fused step with two row pieces per thread: the first half of the fp16
+  // plane, written right after the commit, so that its registers can take
+  // the next head's rows during the pull-back
+  const bool split = fused && DVS * DK / kVT >= 16;
+  s.p0 = split ? size_t(DVS / 2) * (kappa + kSPad) * 2 : 0;
+  s.total = s.rk + s.rv + s.meta + s.p0;
   return s;
 }
 
@@ -440,6 +445,35 @@ __device__ __forceinline__ void store_state_rows(float* S, int b, int Hv, int DV
   }
 }
 
+// Fused step: row piece i of this thread's state elements -> the fp16 plane
+// at base (rows in natural order, stride KS halves), each row scaled by the
+// power of two of row_scale; the inverse scales -> s_rs.
+template <int DK, int DVS, int KS>
+__device__ __forceinline__ void plane_piece(const float (&sr)[FusedSplit<DK, DVS>::EPT], int i, _Float16* base,
+                                            float* s_rs, int tid) {
+  using FS = FusedSplit<DK, DVS>;
+  float m = 0.0f;
+#pragma unroll
+  for (int e = 0; e < FS::CPT; ++e) m = fmaxf(m, fabsf(sr[i * FS::CPT + e]));
+  m = group_max<FS::LPR>(m);
+  float sc, inv;
+  row_scale(m, sc, inv);
+  if (FS::owns(tid)) {
+    const int off = FS::row(tid, i) * KS + FS::col0(tid);
+    if constexpr (FS::CPT % 4 == 0) {
+#pragma unroll
+      for (int e = 0; e < FS::CPT; e += 4)
+        *reinterpret_cast<uint2*>(base + off + e) = to_f16x4(
+            make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1], sr[i * FS::CPT + e + 2], sr[i * FS::CPT + e + 3]),
+            sc);
+    } else {
+#pragma unroll
+      for (int e = 0; e < FS::CPT; ++e) base[off + e] = (_Float16)(sr[i * FS::CPT + e] * sc);
+    }
+    if (FS::col0(tid) == 0) s_rs[FS::row(tid, i)] = inv;
+  }
+}
+
 // Commit (fused step) of the previous step's accepted path (L nodes, slots
 // s_ppath) into the state rows c0 .. c0 + DVS of value head h: features of
 // the path (previous step's raw inputs, conv state before the commit), then
@@ -625,7 +659,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   const int l16 = lane & 15, mlg = lane >> 4;
   const int mpos = l16 < 8 ? base[0] + 2 * l16 : base[1] + 2 * (l16 - 8);
 
-  const VerifySmem L = verify_smem(T, DK, DVS);
+  const VerifySmem L = verify_smem(T, DK, DVS, FUSED);
   float* s_k = reinterpret_cast<float*>(smem);  // q staging, then k~ [TP][KROW]
   unsigned char* s_rv = smem + L.rk;            // k staging / v staging / v~ / S0 planes
   float* s_v = reinterpret_cast<float*>(s_rv);  // [.][VROW]
@@ -638,6 +672,11 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
   float* s_wv = s_wqk + 8 * DK;  // [4][DVS] tap-major
   int* s_ppath = reinterpret_cast<int*>(s_wv + 4 * DVS);  // previous accepted path (fused step)
   float* s_rs = reinterpret_cast<float*>(s_ppath + kVMaxT);  // 1 / row scale of the S0 plane
+  _Float16* s_p0 = reinterpret_cast<_Float16*>(smem + L.rk + L.rv + L.meta);  // plane rows of piece 0 (fused)
+  // fused step, two row pieces per thread: piece 0's plane rows go to s_p0
+  // right after the commit and its registers take the next head's rows
+  // during the pull-back; piece 1 as before
+  constexpr bool kSplit = FUSED && FusedSplit<DK, DVS>::R == 2;
 
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
   const int status = m.status[b];
@@ -846,6 +885,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     // fused step: commit the previous path into this head's state rows (sr
     // then holds the state the tree is verified against)
     if constexpr (FUSED) fused_commit<DK, DVS, TIn>(p, s_rv, s_ppath, Lp, b, g, h, c0, tid, sr);
+    if constexpr (kSplit) plane_piece<DK, DVS, KAPPA + kSPad>(sr, 0, s_p0, s_rs, tid);
     // 2a: raw v rows (prefetched) + 3 conv-state rows -> LDS as fp32
     //     [T + 3][VROW]; gates and v conv weights -> LDS
     const int vch0 = 2 * Hk * DK + h * DV + c0;  // conv channel of v[h][c0]
@@ -950,6 +990,10 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       }
       if constexpr (FUSED)
         if (Lp > 0 && u == 0) store_state_rows<DK, DVS, kSP>(p.S, b, Hv, DV, h, c0, tid, sr, 1);
+      // the next head's rows of piece 0 (stored already, converted at the
+      // head start) load during the deep walk
+      if constexpr (kSplit)
+        if (u == 0 && hh + 1 < p.hpw) load_state_rows<DK, DVS, 2>(p.S, b, Hv, DV, h + 1, c0, tid, sr, 0);
     }
     // a_i x~_i and the value accumulators move to the MFMA layout:
     //   X~^T B operand, k block kb: lane (l16, mlg) holds channels 32 kb + 8 mlg + e
@@ -1075,31 +1119,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     {
       _Float16* s_h = reinterpret_cast<_Float16*>(s_rv);
       if constexpr (FUSED) {
-        using FS = FusedSplit<DK, DVS>;
 #pragma unroll
-        for (int i = 0; i < FS::R; ++i) {
-          float m = 0.0f;
-#pragma unroll
-          for (int e = 0; e < FS::CPT; ++e) m = fmaxf(m, fabsf(sr[i * FS::CPT + e]));
-          m = group_max<FS::LPR>(m);
-          float sc, inv;
-          row_scale(m, sc, inv);
-          if (FS::owns(tid)) {
-            const int off = FS::row(tid, i) * (KAPPA + kSPad) + FS::col0(tid);
-            if constexpr (FS::CPT % 4 == 0) {
-#pragma unroll
-              for (int e = 0; e < FS::CPT; e += 4)
-                *reinterpret_cast<uint2*>(s_h + off + e) =
-                    to_f16x4(make_float4(sr[i * FS::CPT + e], sr[i * FS::CPT + e + 1], sr[i * FS::CPT + e + 2],
-                                         sr[i * FS::CPT + e + 3]),
-                             sc);
-            } else {
-#pragma unroll
-              for (int e = 0; e < FS::CPT; ++e) s_h[off + e] = (_Float16)(sr[i * FS::CPT + e] * sc);
-            }
-            if (FS::col0(tid) == 0) s_rs[FS::row(tid, i)] = inv;
-          }
-        }
+        for (int i = kSplit ? 1 : 0; i < FusedSplit<DK, DVS>::R; ++i)
+          plane_piece<DK, DVS, KAPPA + kSPad>(sr, i, s_h, s_rs, tid);
       } else if constexpr (S0Split<DK, DVS>::kRows) {
         // NS0 float4 of row tid / TPR: one scale per row from a TPR-lane max
         using SP = S0Split<DK, DVS>;
@@ -1144,8 +1166,14 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     __builtin_amdgcn_sched_barrier(0);  // this head's S0 registers are free before the next loads
     // fused step: the next head's state rows load during the MFMA phase
     // (its fused commit at the start of the next head needs them)
-    if constexpr (FUSED)
-      if (hh + 1 < p.hpw) load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
+    if constexpr (FUSED) {
+      if (hh + 1 < p.hpw) {
+        if constexpr (kSplit)
+          load_state_rows<DK, DVS, 2>(p.S, b, Hv, DV, h + 1, c0, tid, sr, 1);
+        else
+          load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
+      }
+    }
     __syncthreads();
 
     // 2e: P^T = (D S0) X~^T on MFMA (fp16 operands, fp32 accumulation);
@@ -1165,7 +1193,8 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         for (int u = 0; u < NP; ++u) {
 #pragma unroll
           for (int kb = 0; kb < KB; ++kb)
-            a[u][kb] = *reinterpret_cast<const f16x8*>(s_h + (16 * (n + u) + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg);
+            a[u][kb] = *reinterpret_cast<const f16x8*>((kSplit && 16 * (n + u) < DVS / 2 ? s_p0 : s_h) +
+                                                       (16 * (n + u) + l16) * (KAPPA + kSPad) + 32 * kb + 8 * mlg);
           rs[u] = *reinterpret_cast<const float4*>(s_rs + 16 * (n + u) + 4 * mlg);
         }
         f32x4 d[NP];
@@ -1234,12 +1263,12 @@ static int launch_verify_t(const VerifyArgs& a, int hpw, int ns, hipStream_t str
   p.conv_state_out = a.conv_state_out;
   p.S = a.S;
   p.commit_status = a.commit_status;
-  const size_t smem = verify_smem(a.T, DK, DVS).total;
+  const size_t smem = verify_smem(a.T, DK, DVS, FUSED).total;
   static bool attr_done = false;
   if (!attr_done) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&verify_kernel<DK, DVS, TIn, FUSED>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(verify_smem(kVMaxT, DK, DVS).total));
+                                       int(verify_smem(kVMaxT, DK, DVS, FUSED).total));
     if (e != hipSuccess)
       return set_error(GDN_EHIP, "verify: LDS attribute: %s", hipGetErrorString(e));
     attr_done = true;
