@@ -171,6 +171,15 @@ __device__ __forceinline__ void split4(float4 x, uint2& hi, uint2& lo) {
   lo = make_uint2((l[0] >> 16) | l[1], (l[2] >> 16) | l[3]);
 }
 
+// Workgroup barrier that orders LDS accesses only: global loads and stores
+// issued before it stay in flight (a full __syncthreads waits for all of
+// them).  No thread here reads global memory another thread writes.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Pins x to a register at this point: keeps the compiler from sinking the
 // arithmetic that produces it past a later barrier (which would keep every
 // operand it reads alive across the barrier).
@@ -1174,7 +1183,20 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
           load_state_rows<DK, DVS>(p.S, b, Hv, DV, h + 1, c0, tid, sr);
       }
     }
-    __syncthreads();
+    // the next head's raw values and gates load ahead of this head's output
+    // stores: loads and stores complete in issue order, so the wait for
+    // them at the next head's start then does not wait for the stores,
+    // which drain behind the next head's work (the barriers below order LDS
+    // only)
+    if (hh + 1 < p.hpw) {
+      prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
+      if constexpr (FUSED)
+        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
+                 static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
+      else
+        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
+    }
+    lds_barrier();
 
     // 2e: P^T = (D S0) X~^T on MFMA (fp16 operands, fp32 accumulation);
     //     O^T = scale (D^-1 P^T + ACC^T) in the accumulator layout; store
@@ -1211,23 +1233,10 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
             *reinterpret_cast<float4*>(orow_p + 16 * t + 4 * mlg) =
                 make_float4(p.scale * fmaf(d[u][0], rs[u].x, am[t][0]), p.scale * fmaf(d[u][1], rs[u].y, am[t][1]),
                             p.scale * fmaf(d[u][2], rs[u].z, am[t][2]), p.scale * fmaf(d[u][3], rs[u].w, am[t][3]));
-          // the next head's raw values and gates load tile by tile behind
-          // the output stores
-          if (hh + 1 < p.hpw) {
-            prefetch_v<TIn, DVS, NVC, NT>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid,
-                                          vpf, t);
-            if (t == NT - 1) {
-              if constexpr (FUSED)
-                gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
-                         static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
-              else
-                gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
-            }
-          }
         }
       }
     }
-    __syncthreads();  // S0 planes consumed before the next head reuses the region
+    lds_barrier();  // S0 planes consumed before the next head reuses the region
   }
   if constexpr (FUSED)
     fused_conv_out<DK, DVS, TIn>(p, s_ppath, Lp, b, g, h0, c0, blockIdx.x == 0 && blockIdx.y % nhg == 0, tid);
