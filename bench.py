@@ -161,7 +161,7 @@ def main() -> int:
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): every "
-              "(sequence, head) unit is independent and this build has no multi-GPU path.",
+              "(sequence, head) unit is independent and there is no multi-GPU path.",
               file=sys.stderr)
         return 2
 

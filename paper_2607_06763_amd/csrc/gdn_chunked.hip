@@ -243,11 +243,11 @@ __global__ __launch_bounds__(kQT) void chunked_verify_kernel(ChunkParams p) {
   const TIn* beta = static_cast<const TIn*>(p.beta);
 
   // ---------------- phase 0: metadata, gates, conv weights and state ----------------
-  // Round 1 issues every load that does not depend on the tree (status,
-  // order / depth / parent position, conv weights and state, S0); round 2
-  // the gates and ancestor words of the node at each position together with
-  // the raw q / k / v rows of the conv taps.  The status is tested after
-  // round 1 (every address is valid whatever the status).
+  // The first load wave issues every load that does not depend on the tree
+  // (status, order / depth / parent position, conv weights and state, S0);
+  // the second the gates and ancestor words of the node at each position
+  // together with the raw q / k / v rows of the conv taps.  The status is
+  // tested after the first wave (every address is valid whatever the status).
   const int status = mp.status[b];
   const int nv = mp.nvalid[b];
   int node = 0, pdep = -1, pp = -1;
@@ -297,7 +297,7 @@ __global__ __launch_bounds__(kQT) void chunked_verify_kernel(ChunkParams p) {
     s_wk[tid] = wkv;
   }
   if (tid < 4 * DV) s_wv[tid] = wvv;
-  // round 2, part 1: gates and ancestor words of the node at position tid
+  // second load wave, part 1: gates and ancestor words of the node at position tid
   TIn g_al = TIn(), g_be = TIn();
   uint64_t g_a0 = 0ull, g_a1 = 0ull;
   if (tid < kQMaxT) {
@@ -314,7 +314,7 @@ __global__ __launch_bounds__(kQT) void chunked_verify_kernel(ChunkParams p) {
   }
   __syncthreads();  // order, depth, parent positions, conv weights / state in LDS
 
-  // round 2, part 2: the conv tap rows of the own node (position
+  // second load wave, part 2: the conv tap rows of the own node (position
   // pos = 16 blk + r, channels 32 g + 8 m + e)
   const bool preal = owner && pos < nv;
   int tnode[4], tcs[4];

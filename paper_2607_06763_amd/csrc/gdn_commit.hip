@@ -75,7 +75,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
   const TIn* alpha = static_cast<const TIn*>(p.alpha);
   const TIn* beta = static_cast<const TIn*>(p.beta);
 
-  // ---- first round: statuses, depths and gates of all slots (raw gates are
+  // ---- first load wave: statuses, depths and gates of all slots (raw gates are
   //      converted only once the path is known)
   const int a = p.accepted[b];
   const int tree_st = m.status[b];
@@ -88,7 +88,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
       p.commit_status[b] = tree_st != GDN_TREE_OK ? tree_st : (a == -1 ? GDN_TREE_OK : GDN_TREE_BAD_ACCEPTED);
     return;
   }
-  // ---- second round: the ancestor bitmask of a -> the path root..a
+  // ---- second load wave: the ancestor bitmask of a -> the path root..a
   const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (tj >> 6)];
   if (tid < T) s_dep[tid] = dep_j;
   __syncthreads();

@@ -9,7 +9,7 @@
 * closed forms: beta = 0 (pure decay, the diagonal case of Sec. 2.2.5),
   alpha = beta = 1 with q = k (delta-rule write: o = scale v);
 * a chain tree equals sequential decoding written in the stored [dv][dk]
-  orientation, including two verify/commit rounds (conv-state shift);
+  orientation, including two verify/commit steps (conv-state shift);
 * node locality and relabelling invariance of the tree semantics.
 
 Shapes use dk != dv so that a transposed operand cannot pass unnoticed.
@@ -257,7 +257,7 @@ def test_chain_equals_sequential_decode(orc):
         np.testing.assert_allclose(out[0, :, h], o, rtol=1e-12, atol=1e-14)
 
 
-def test_two_rounds_equal_sequential_decode(orc):
+def test_two_steps_equal_sequential_decode(orc):
     """verify/commit on chain 1 (accept node 3), then verify on chain 2 from the
     committed state and conv state == decoding the 4 + 6 tokens in sequence."""
     w1 = _small(80, W.chain_tree(7))
@@ -265,7 +265,7 @@ def test_two_rounds_equal_sequential_decode(orc):
     w2 = _small(81, W.chain_tree(6))
     S1, cs1, st = orc.commit(w1)
     assert st[0] == 0
-    w2.conv_w = w1.conv_w.copy()   # same layer weights in both rounds
+    w2.conv_w = w1.conv_w.copy()   # same layer weights in both steps
     w2.S0 = S1.astype(np.float64)
     w2.conv_state = cs1
     out2 = orc.verify(w2)
@@ -280,7 +280,7 @@ def test_two_rounds_equal_sequential_decode(orc):
         be = np.concatenate([_f64(w1, "beta")[0, :4, h], _f64(w2, "beta")[0, :, h]])
         o, _ = _decode(_f64(w1, "S0")[0, h], feats, al, be, w1, h)
         np.testing.assert_allclose(out2[0, :, h], o[4:], rtol=1e-11, atol=1e-13)
-    # conv state after round 1 = raw inputs of chain nodes 1, 2, 3
+    # conv state after the first step = raw inputs of chain nodes 1, 2, 3
     np.testing.assert_array_equal(cs1[0], _raw_channels(w1, 0)[1:4])
 
 
