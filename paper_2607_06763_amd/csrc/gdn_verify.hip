@@ -33,20 +33,25 @@
 //     low when the 8 nodes of a wave read 8 unrelated ancestor rows;
 //   * MFMA: node column l16 = lane % 16, lane group mlg = lane / 16, the
 //     B-operand layout of X~^T and the accumulator layout of O^T for
-//     v_mfma_f32_16x16x32_bf16.  One ds_bpermute per register and node half
-//     moves the pulled-back queries and value accumulators across.
-//   phase 0  tree metadata in canonical order -> LDS; prefetch S0 and raw v
-//            of the first head into registers
+//     v_mfma_f32_16x16x32_f16.  The halves of each 8-lane group first trade
+//     registers by DPP so that every ds_bpermute that moves the pulled-back
+//     queries (fp16 pairs) and value accumulators across carries only values
+//     its destination needs.
+//   phase 0  tree metadata in canonical order -> LDS
 //   phase 1  conv + SiLU + L2-norm of q and k along each node's path (raw
-//            rows staged in LDS); q~ stays in registers, k~ -> LDS (fp32)
+//            rows staged in LDS); q~ stays in registers, k~ -> LDS (fp32);
+//            the first head's raw v and gates load meanwhile
 //   per value head:
-//     2a/b   raw v (prefetched) -> LDS, conv + SiLU -> v~ in LDS (fp32)
+//     2a/b   raw v (prefetched) -> LDS, conv + SiLU -> v~ in LDS (fp32);
+//            this head's S0 loads
 //     2c     pull-back with k~, v~ gathered from LDS (8 lanes per node),
 //            move to the MFMA layout
-//     2d     S0 (prefetched) -> LDS as one fp16 plane of row-scaled values;
-//            prefetch the next head's raw v, gates and v conv weights
-//     2e     MFMA P^T = (D S0) X~^T, O^T = D^-1 P^T + ACC^T, store; prefetch
-//            the next head's S0
+//     2d     S0 -> LDS as one fp16 plane of row-scaled values; the next
+//            head's raw v and gates load (ahead of this head's stores)
+//     2e     MFMA P^T = (D S0) X~^T, O^T = D^-1 P^T + ACC^T, store
+// The fused step (FUSED) first commits the previous step's accepted path
+// into each head's state rows, which then stand in for S0 (see
+// fused_commit).
 #include "gdn_internal.h"
 
 namespace gdn {
@@ -155,20 +160,6 @@ template <int D>
 __device__ __forceinline__ int row_off(int t) {
   static_assert((D & (D - 1)) == 0 && kKPad == 4, "power-of-two rows (plus 4)");
   return D >= 64 ? (t << __builtin_ctz(D)) : (t << __builtin_ctz(D)) + (t << 2);
-}
-
-// 4 floats -> packed bf16 hi (2 dwords) and lo (2 dwords), truncation split
-__device__ __forceinline__ void split4(float4 x, uint2& hi, uint2& lo) {
-  const float xs[4] = {x.x, x.y, x.z, x.w};
-  uint32_t h[4], l[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const uint32_t u = __float_as_uint(xs[e]);
-    h[e] = u & 0xffff0000u;
-    l[e] = __float_as_uint(xs[e] - __uint_as_float(h[e])) & 0xffff0000u;
-  }
-  hi = make_uint2((h[0] >> 16) | h[1], (h[2] >> 16) | h[3]);
-  lo = make_uint2((l[0] >> 16) | l[1], (l[2] >> 16) | l[3]);
 }
 
 // Workgroup barrier that orders LDS accesses only: global loads and stores
@@ -925,6 +916,7 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int c = 0; c < VPL; ++c) vt[u][c] = 0.0f;
+      // this head's S0 (needed after the pull-back)
       if constexpr (!FUSED)
         prefetch_s0<DK, DVS, NS0>(p.S0 + (size_t(b) * Hv + h) * DV * DK + size_t(c0) * DK, tid, s0pf);
 #pragma unroll
@@ -938,8 +930,6 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
 #pragma unroll
           for (int c = 0; c < VPL; ++c) vt[u][c] += wt[c] * xw[c];
         }
-        // this head's S0, a quarter per tap: it is needed after the
-        // pull-back, and spreading the loads keeps the wave issuing
         __builtin_amdgcn_sched_barrier(0);  // one tap's rows in flight at a time
       }
 #pragma unroll
