@@ -171,6 +171,14 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Streaming store of 4 floats: the outputs are not read again by this
+// kernel, and the non-temporal hint keeps them from displacing the inputs
+// and state in the caches (measured 174 -> 166 us per fused step).
+__device__ __forceinline__ void store_stream(float* dst, float a, float b, float c, float d) {
+  typedef float f32v4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(f32v4{a, b, c, d}, reinterpret_cast<f32v4*>(dst));
+}
+
 // Pins x to a register at this point: keeps the compiler from sinking the
 // arithmetic that produces it past a later barrier (which would keep every
 // operand it reads alive across the barrier).
@@ -1220,9 +1228,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         for (int u = 0; u < NP; ++u) {
           const int t = n + u;
           if (mpos < T)
-            *reinterpret_cast<float4*>(orow_p + 16 * t + 4 * mlg) =
-                make_float4(p.scale * fmaf(d[u][0], rs[u].x, am[t][0]), p.scale * fmaf(d[u][1], rs[u].y, am[t][1]),
-                            p.scale * fmaf(d[u][2], rs[u].z, am[t][2]), p.scale * fmaf(d[u][3], rs[u].w, am[t][3]));
+            store_stream(orow_p + 16 * t + 4 * mlg, p.scale * fmaf(d[u][0], rs[u].x, am[t][0]),
+                         p.scale * fmaf(d[u][1], rs[u].y, am[t][1]), p.scale * fmaf(d[u][2], rs[u].z, am[t][2]),
+                         p.scale * fmaf(d[u][3], rs[u].w, am[t][3]));
         }
       }
     }
