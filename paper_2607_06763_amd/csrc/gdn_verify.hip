@@ -184,6 +184,15 @@ __device__ __forceinline__ void store_stream(float* dst, float a, float b, float
 // operand it reads alive across the barrier).
 __device__ __forceinline__ void pin(float& x) { asm volatile("" : "+v"(x)); }
 
+// The thread index as a value the compiler cannot see through: addresses
+// derived from it are computed where they are used instead of being hoisted
+// out of the head loop and held in registers across it (which spills, and a
+// spill reload waits for every vector memory operation issued before it).
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // Value of v held by lane src of this wave (ds_bpermute).
 __device__ __forceinline__ float lane_gather(float v, int src) {
   return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
@@ -1187,12 +1196,13 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
     // which drain behind the next head's work (the barriers below order LDS
     // only)
     if (hh + 1 < p.hpw) {
-      prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, tid, vpf);
+      const int otid = opaque(tid);
+      prefetch_v<TIn, DVS>(vin + size_t(b) * T * orow + size_t(h + 1) * DV + c0, orow, s_ord, T, otid, vpf);
       if constexpr (FUSED)
-        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid,
+        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, otid,
                  static_cast<const TIn*>(p.pv), orow, (h + 1) * DV + c0, s_ppath, Lp);
       else
-        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, tid);
+        gpf.load(alpha, beta, p.conv_w, p.conv_state, s_ord, b, T, Hv, C, h + 1, vch0 + DV, otid);
     }
     lds_barrier();
 
