@@ -516,11 +516,9 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
   float* s_inv = s_fv + kMC * DVS;              // [kMC] 1 / ||k||
   float* s_al = s_inv + kMC;                    // [kVMaxT] gates by path index
   float* s_be = s_al + kVMaxT;
-  // gates of path node tid (tid < L; clamped loads, stored with the first
-  // chunk's features so that one wait covers both)
+  // gates of path node tid (tid < L): loaded with the first chunk's window
+  // and stored with its features, so that one wait covers both
   const size_t gab = (size_t(b) * T + s_ppath[tid < L ? tid : 0]) * Hv + h;
-  const TIn gal = static_cast<const TIn*>(p.palpha)[gab];
-  const TIn gbe = static_cast<const TIn*>(p.pbeta)[gab];
   // feature task of this thread: value channel of the slice (tid < FP DVS)
   // or key channel (FP DVS <= tid < FP (DVS + DK)); fpart picks the part
   const bool vtask = tid < FP * DVS;
@@ -538,9 +536,10 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
   for (int base = 0; base < L; base += kMC) {
     FeatWindow<TIn, FN> win;
     if (vtask || ktask) win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_ppath, base + fpart * FN, L);
-    if (base == 0 && tid < L) {
-      s_al[tid] = to_f32(gal);
-      s_be[tid] = to_f32(gbe);
+    TIn gal, gbe;
+    if (base == 0) {  // clamped loads, issued after the window's
+      gal = static_cast<const TIn*>(p.palpha)[gab];
+      gbe = static_cast<const TIn*>(p.pbeta)[gab];
     }
     if (vtask || ktask) {
       const int m0 = base + fpart * FN;
@@ -553,6 +552,10 @@ __device__ __forceinline__ void fused_commit(const VerifyParams& p, unsigned cha
         else
           s_fk[(fpart * FN + mr) * DK + fc] = y;
       }
+    }
+    if (base == 0 && tid < L) {
+      s_al[tid] = to_f32(gal);
+      s_be[tid] = to_f32(gbe);
     }
     __syncthreads();
     // key norms: 16 lanes per path node, DK / 16 channels per lane
