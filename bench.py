@@ -11,10 +11,13 @@ separate launches, prepare / verify / commit).
 The default workload is the large one: 32 trees of 128 nodes (depth 16),
 16 key / 48 value heads, dk = dv = 128, bf16 inputs, fp32 state.
 
-The timed steps run eagerly first (HIP events around every launch give the
-per-kernel durations), then two consecutive steps are captured in a HIP graph
-and replayed (the tree shapes are fixed, so the pass is captured once); the
-replay time is the step time (--no-graph: the eager time).
+The timed steps run eagerly (HIP events around every launch give the
+per-kernel durations) with cold caches: a 512 MiB buffer is written before
+every step (warm-up included), outside its events, so that L2 and the MALL
+hold nothing the step reads, as in a model whose other layers run between two
+steps of this one; the step time is the sum of its kernels' times.  --hot: no
+eviction, and two consecutive steps are captured in a HIP graph and replayed
+back to back; the replay time is the step time (--no-graph: the eager time).
 
 Prints ONE JSON line on stdout: throughput in tree nodes verified per second
 per GDN layer, the roofline of the dominant kernel (the fused step, or verify
@@ -150,6 +153,11 @@ def main() -> int:
     ap.add_argument("--chunked", action="store_true",
                     help="verify with the chunked-form kernel (Eq. 9-13) instead of the pull-back; "
                          "implies --unfused")
+    ap.add_argument("--hot", action="store_true",
+                    help="back-to-back steps on warm caches: kernel times from eager steps, value from "
+                         "the HIP-graph replay (default: cold, a 512 MiB buffer is written before every "
+                         "step, outside its events, evicting L2 and the MALL; kernel times and value "
+                         "from those steps)")
     ap.add_argument("--unfused", action="store_true",
                     help="time prepare, verify and commit as three launches (default: prepare + "
                          "the fused commit-then-verify step)")
@@ -217,15 +225,23 @@ def main() -> int:
         if ev is not None:
             ev[3].record()
 
+    cold = not args.hot
+    flush = torch.empty((512 << 20) // 4, dtype=torch.float32, device="cuda:0") if cold else None
+    if cold:
+        args.graph = False  # every launch of a cold run sees cold caches
     if fused:
         G.prepare(dt.dims, dt.parent, metas[1], dt.tree_status)  # the "previous" tree of step 0
     for i in range(args.warmup):
+        if flush is not None:
+            flush.fill_(float(i))
         step(i)
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        if flush is not None:
+            flush.fill_(float(i))
         step(args.warmup + i, events[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -264,6 +280,8 @@ def main() -> int:
         us_prep, us_main, us_com = (float(x) for x in per.mean(0))
         kname, kbytes = ("verify_chunked" if args.chunked else "verify"), nbytes["verify"]
     p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
+    if cold:  # the eager wall time includes the flushes: the kernels' own times
+        ms_step = float(per.sum(1).mean()) * 1e-3
     ach = kbytes / (us_main * 1e-6) / 1e9
     traffic = measured_traffic(src_hash, kname, w.name)
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -289,6 +307,9 @@ def main() -> int:
                 / HBM_PEAK_GBS, 4),
         }
     detail["algorithmic_bytes"] = nbytes
+    detail["caches"] = ("cold: 512 MiB written before every timed step (outside its events); value = nodes / "
+                        "the mean of the step's kernel times" if cold else
+                        "hot: back-to-back steps" + ("; value from the HIP-graph replay" if args.graph else ""))
     if args.graph:
         detail["ms_per_step_eager"] = round(ms_eager, 5)
     detail["verify_source_sha256_16"] = src_hash
@@ -309,7 +330,7 @@ def main() -> int:
                                f"dk={w.dk} dv={w.dv}, {w.in_dtype} inputs, fp32 state and output",
                    "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)",
                    "step": ("prepare + fused commit/verify" if fused else
-                            "prepare + " + ("chunked " if args.chunked else "") + "verify + commit") + (", HIP graph replay" if args.graph else "")},
+                            "prepare + " + ("chunked " if args.chunked else "") + "verify + commit") + (", HIP graph replay" if args.graph else ", cold caches" if cold else "")},
         "roofline": roofline,
         "detail": detail,
     }
