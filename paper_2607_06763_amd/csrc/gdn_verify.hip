@@ -171,12 +171,13 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Streaming store of 4 floats: the outputs are not read again by this
-// kernel, and the non-temporal hint keeps them from displacing the inputs
-// and state in the caches (measured 174 -> 166 us per fused step).
-__device__ __forceinline__ void store_stream(float* dst, float a, float b, float c, float d) {
-  typedef float f32v4 __attribute__((ext_vector_type(4)));
-  __builtin_nontemporal_store(f32v4{a, b, c, d}, reinterpret_cast<f32v4*>(dst));
+// Streaming load of 16 bytes (the raw q, k, v rows, read once per launch):
+// the non-temporal hint keeps them from displacing the state rows in the
+// caches.
+__device__ __forceinline__ uint4 load_stream(const void* src) {
+  typedef unsigned u32v4 __attribute__((ext_vector_type(4)));
+  const u32v4 v = __builtin_nontemporal_load(reinterpret_cast<const u32v4*>(src));
+  return make_uint4(v.x, v.y, v.z, v.w);
 }
 
 // Pins x to a register at this point: keeps the compiler from sinking the
@@ -312,7 +313,7 @@ __device__ __forceinline__ void prefetch_v(const TIn* vin, size_t node_stride, c
     if (j % PARTS != part) continue;
     const int idx = j * kVT + tid;
     const int p = idx / CPR < T ? idx / CPR : T - 1, c = idx % CPR;  // rows >= T are never stored
-    pf[j] = *reinterpret_cast<const uint4*>(vin + size_t(s_ord[p]) * node_stride + c * EPC);
+    pf[j] = load_stream(vin + size_t(s_ord[p]) * node_stride + c * EPC);
   }
 }
 
@@ -781,8 +782,8 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
       const int row = idx / QCPR, c = (idx % QCPR) * EPC;
       if (row < T) {
         const size_t off = size_t(s_ord[row]) * qk_row + c;
-        qpf[j] = *reinterpret_cast<const uint4*>(qsrc + off);
-        kpf[j] = *reinterpret_cast<const uint4*>(ksrc + off);
+        qpf[j] = load_stream(qsrc + off);
+        kpf[j] = load_stream(ksrc + off);
       }
     }
     float* s_kst = reinterpret_cast<float*>(s_rv);
@@ -1241,9 +1242,9 @@ __global__ __launch_bounds__(kVT) void verify_kernel(VerifyParams p) {
         for (int u = 0; u < NP; ++u) {
           const int t = n + u;
           if (mpos < T)
-            store_stream(orow_p + 16 * t + 4 * mlg, p.scale * fmaf(d[u][0], rs[u].x, am[t][0]),
-                         p.scale * fmaf(d[u][1], rs[u].y, am[t][1]), p.scale * fmaf(d[u][2], rs[u].z, am[t][2]),
-                         p.scale * fmaf(d[u][3], rs[u].w, am[t][3]));
+            *reinterpret_cast<float4*>(orow_p + 16 * t + 4 * mlg) =
+                make_float4(p.scale * fmaf(d[u][0], rs[u].x, am[t][0]), p.scale * fmaf(d[u][1], rs[u].y, am[t][1]),
+                            p.scale * fmaf(d[u][2], rs[u].z, am[t][2]), p.scale * fmaf(d[u][3], rs[u].w, am[t][3]));
         }
       }
     }
