@@ -21,7 +21,7 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
                                                             int T) {
   __shared__ int s_par[kPrepMaxT];
   __shared__ int s_nxt[kPrepMaxT];
-  __shared__ int s_dep[kPrepMaxT];
+  __shared__ __align__(16) int s_dep[kPrepMaxT];
   __shared__ uint64_t s_anc[kPrepMaxT * kPrepMaxW];
   __shared__ int s_bad, s_roots, s_real, s_cycle;
 
@@ -110,15 +110,22 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
     return;
   }
 
-  // canonical order: rank by key (depth, index); padding keyed after all depths
-  if (slot) s_dep[i] = real ? dep : T + 1;
+  // canonical order: rank by key (depth, index); padding keyed after all
+  // depths; the keys are read four at a time (slots T .. up to a multiple of
+  // 4 hold a key above every real one, so they never count)
+  const int T4 = (T + 3) & ~3;
+  if (i < T4) s_dep[i] = slot ? (real ? dep : T + 1) : 0x7fffffff;
   __syncthreads();
   if (slot) {
     const int key = s_dep[i];
     int rank = 0;
-    for (int j = 0; j < T; ++j) {
-      int kj = s_dep[j];
-      rank += (kj < key) || (kj == key && j < i);
+#pragma unroll 4
+    for (int j = 0; j < T4; j += 4) {
+      const int4 k4 = *reinterpret_cast<const int4*>(s_dep + j);
+      rank += (k4.x < key) || (k4.x == key && j < i);
+      rank += (k4.y < key) || (k4.y == key && j + 1 < i);
+      rank += (k4.z < key) || (k4.z == key && j + 2 < i);
+      rank += (k4.w < key) || (k4.w == key && j + 3 < i);
     }
     m.order[base + rank] = i;
     m.pos[base + i] = rank;
