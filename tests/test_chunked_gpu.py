@@ -1,10 +1,8 @@
 """GPU parity of the chunked-form verification (gdn_tree_verify_chunked,
-Sec. 3.4.1 Eq. 9-13) against the CPU oracle, and against the pull-back
-verification on the device.
+Sec. 3.4.1 Eq. 9-13) against the CPU oracle.
 
 Bars: max|o - o_ref| <= 2e-3 max|o_ref|; invalid trees and padding slots give
-zero rows; S0 and the conv state stay bit-identical.  The large workload is
-checked on sampled nodes."""
+zero rows; S0 and the conv state stay bit-identical."""
 import numpy as np
 import pytest
 
@@ -52,27 +50,13 @@ def test_chunked_named_full(G, orc, cfg):
     assert err <= O_TOL
 
 
-def test_chunked_large_sampled_and_vs_pullback(G, orc):
-    import torch
+def test_chunked_large_full(G, orc):
     w = W.make_config(4)
-    _announce("chunked cfg=4 (sampled) and against the pull-back")
-    dt, got = _run(G, w)
-    mask = np.zeros((w.B, w.T), np.uint8)
-    rng = np.random.default_rng(11)
-    for b in range(w.B):
-        mask[b, rng.choice(w.T, 3, replace=False)] = 1
-        mask[b, int(w.accepted[b])] = 1
-    ref = orc.verify(w, node_mask=mask)
-    sel = mask.astype(bool)
-    err = _out_err(got[sel], ref[sel])
-    _announce(f"  sampled err {err:.3e}")
+    _announce("chunked cfg=4 (all nodes)")
+    _dt, got = _run(G, w)
+    err = _out_err(got, orc.verify(w))
+    _announce(f"  err {err:.3e}")
     assert err <= O_TOL
-    dt.verify(chunked=False)
-    torch.cuda.synchronize()
-    pb = dt.out.cpu().numpy().astype(np.float64)
-    err2 = _out_err(got, pb)
-    _announce(f"  chunked vs pull-back {err2:.3e}")
-    assert err2 <= 1e-4
 
 
 def test_chunked_unsupported_head_dim(G):

@@ -4,7 +4,7 @@ Bars: tree metadata, statuses and the conv state are bit-exact; verify
 outputs satisfy max|o - o_ref| <= 2e-3 * max|o_ref|; the committed fp32
 state satisfies ||S - S_ref||_F <= 1e-4 ||S_ref||_F for every
 (sequence, value head).  The large workload (32 x 128-node trees, 48 value
-heads) is checked on sampled nodes, which the oracle evaluates one by one.
+heads) is checked on every node.
 """
 import numpy as np
 import pytest
@@ -45,13 +45,25 @@ def _check_meta(G, dt, w, orc):
     for b in range(B):
         if ref["status"][b] != 0:
             assert (got["pdep"][b] == -1).all() and (got["ppos"][b] == -1).all()
+            assert (got["ancp"][b] == 0).all() and (got["qoff"][b] == 0).all()
             continue
         pos = np.argsort(ref["order"][b])
+        W_ = ref["anc"].shape[2]
+        qoff = 0
         for p_ in range(T):
             node = ref["order"][b, p_]
             assert got["pdep"][b, p_] == ref["depth"][b, node]
             par = w.parent[b, node]
             assert got["ppos"][b, p_] == (pos[par] if par >= 0 else -1)
+            # ancestor set in position space, and the ragged-table offsets
+            want = np.zeros(W_, np.uint64)
+            for j in range(T):
+                if (int(ref["anc"][b, node, j // 64]) >> (j % 64)) & 1:
+                    want[pos[j] // 64] |= np.uint64(1 << (pos[j] % 64))
+            np.testing.assert_array_equal(got["ancp"][b, p_], want)
+            assert got["qoff"][b, p_] == qoff
+            qoff += ref["depth"][b, node] + 1 if ref["depth"][b, node] >= 0 else 0
+        assert got["qoff"][b, T] == qoff
     np.testing.assert_array_equal(got["parent"], w.parent)
     np.testing.assert_array_equal(dt.tree_status.cpu().numpy(), ref["status"])
 
@@ -115,15 +127,16 @@ def test_verify_named_full(G, orc, cfg):
     assert err <= O_TOL
 
 
-def test_verify_large_sampled(G, orc):
+def test_verify_large_full(G, orc):
+    """The large workload (32 trees x 128 nodes, 16 key / 48 value heads,
+    d = 128): every node of every head against the oracle.  This is the
+    grouped grid (all value heads of a key head in one workgroup)."""
     w = W.make_config(4)
-    _announce(f"verify cfg=4 B={w.B} T={w.T} Hv={w.Hv} (sampled)")
+    _announce(f"verify cfg=4 B={w.B} T={w.T} Hv={w.Hv} (all nodes)")
     _dt, got = _run_verify(G, w)
-    mask = _sample_mask(w, 2, 7)
-    ref = orc.verify(w, node_mask=mask)
-    sel = mask.astype(bool)
-    err = _out_err(got[sel], ref[sel])
-    _announce(f"  {sel.sum()} nodes, max|err|/max|ref| = {err:.3e}")
+    ref = orc.verify(w)
+    err = _out_err(got, ref)
+    _announce(f"  max|err|/max|ref| = {err:.3e}")
     assert err <= O_TOL
     assert np.isfinite(got).all()
 
@@ -176,6 +189,8 @@ SHAPES = [
     (2, 128, 1, 2, 128, 128, "bf16", [128, 97], None),
     (1, 128, 1, 1, 32, 32, "f32", None, None),   # deep random tree
     (4, 17, 4, 8, 64, 64, "bf16", [17, 0, 3, 16], 3),  # includes an empty tree
+    # B * Hk >= 256: every value head of a key head in one workgroup
+    (128, 20, 2, 6, 32, 32, "bf16", [20, 0] + [20 - (i % 7) for i in range(126)], None),
 ]
 
 

@@ -6,8 +6,7 @@ Reference: the oracle's commit of the previous step, then the oracle's verify
 of the current tree on the committed state and conv state (Sec. 3.4-3.4.2).
 Bars as for the separate entry points: statuses and the conv state
 bit-exact, outputs within 2e-3 max|o_ref|, the committed state within 1e-4
-relative Frobenius per (sequence, value head).  The fused step is also
-compared with the device's own commit-then-verify.
+relative Frobenius per (sequence, value head), on every node.
 """
 import numpy as np
 import pytest
@@ -77,18 +76,6 @@ def _reference(orc, wp, wc, node_mask=None):
     return S_ref, cs_ref, st, out_ref
 
 
-def _unfused(G, dp, dc):
-    """The device's separate commit, then verify, on copies of the inputs."""
-    import torch
-    S = dp.S0.clone()
-    cs = dp.conv_state.clone()
-    dp.commit(S, cs)
-    out = torch.full_like(dc.out, float("nan"))
-    dc.verify(S0=S, conv_state=cs, out=out)
-    torch.cuda.synchronize()
-    return S.cpu().numpy(), cs.cpu().numpy(), out.cpu().numpy()
-
-
 def _check(got, ref, mask=None):
     S_ref, cs_ref, st, out_ref = ref
     np.testing.assert_array_equal(got["status"], st)
@@ -105,29 +92,16 @@ def _check(got, ref, mask=None):
 def test_step_large(G, orc):
     """32 sequences, 16 key / 48 value heads, d = 128, 128-node trees: the
     previous step is the large named workload, the current one a fresh tree
-    set of the same recipe; outputs checked on sampled nodes, and against the
-    device's separate commit + verify."""
+    set of the same recipe; every node of every head is checked."""
     wp = W.make_config(4)
     rng = np.random.default_rng(77)
     par = np.stack([W.random_depth_capped_tree(rng, 128, 15, spine=16, max_children=8)
                     for _ in range(32)])
     wc = W.make_random(4077, 32, 128, 16, 48, 128, 128, "bf16", parent=par)
     wc.conv_w = wp.conv_w
-    _announce("step large B=32 T=128 Hk=16 Hv=48 d=128")
+    _announce("step large B=32 T=128 Hk=16 Hv=48 d=128 (all nodes)")
     got = _run_step(G, wp, wc)
-    mask = np.zeros((32, 128), np.uint8)
-    mrng = np.random.default_rng(5)
-    for b in range(32):
-        mask[b, mrng.choice(128, 3, replace=False)] = 1
-        mask[b, int(wc.accepted[b])] = 1
-    ref = _reference(orc, wp, wc, node_mask=mask)
-    _check(got, ref, mask)
-    # the separate kernels round the features in a different order (FMA
-    # contraction), so the two device paths agree to a few ulp, not bit for bit
-    S2, cs2, out2 = _unfused(G, got["dp"], got["dc"])
-    np.testing.assert_array_equal(got["cs"], cs2)
-    assert _state_err(got["S"], S2.astype(np.float64)) <= 1e-6
-    assert _out_err(got["out"].astype(np.float64), out2.astype(np.float64)) <= 1e-5
+    _check(got, _reference(orc, wp, wc))
 
 
 STEP_SHAPES = [
@@ -139,6 +113,7 @@ STEP_SHAPES = [
     (2, 100, 3, 3, 16, 64, "bf16", [100, 71], 12),
     (2, 128, 1, 2, 128, 128, "bf16", [128, 97], None),
     (4, 17, 4, 8, 64, 64, "bf16", [17, 0, 3, 16], 3),  # includes an empty tree
+    (128, 20, 2, 6, 32, 32, "bf16", [20, 0] + [20 - (i % 7) for i in range(126)], None),
 ]
 
 
