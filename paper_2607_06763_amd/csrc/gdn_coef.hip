@@ -102,8 +102,11 @@ struct CoefMeta {
   float al[kCMaxT], be[kCMaxT];  // gates by position (this head)
   float wv[4][kCD];    // v conv weights of this head, tap-major
   float rs[kCD];       // inverse power-of-two scale of each state row
+  float rsv[kCD];      // inverse power-of-two scale of each v~ channel
+  float4 gt[kCMaxT];   // per position: beta, alpha, start of its G-table row
   int ppath[kCMaxT];   // committed path, root first (slots of the commit tree)
   float pal[kCMaxT], pbe[kCMaxT], psuf[kCMaxT];  // its gates; suffix products
+  float cso[3][kCD];   // conv-state slots before the commit (v channels of this head)
   int misc[16];
 };
 
@@ -119,18 +122,21 @@ __host__ __device__ inline CoefSmem coef_smem(int T, int mode, int in_bytes) {
   const int NT = (T + 15) / 16;
   s.TR = 32 * ((T + 31) / 32);
   const size_t meta = (sizeof(CoefMeta) + 255) & ~size_t(255);
-  const size_t tab = mode == kModeCommit ? 0 : ((2 * size_t(T) * T + 255) & ~size_t(255));
-  const size_t kp = mode == kModeVerify ? 0 : ((size_t(kPC) * kKpRow * 4 + size_t(kPC) * kGpRow * 4 + 255) & ~size_t(255));
+  // ragged tables (T^2 entries at most) or fixed rows (2 x kDRow T)
+  const size_t tab_entries = size_t(T) * T > 2 * 66 * size_t(T) ? size_t(T) * T : 2 * 66 * size_t(T);
+  const size_t tab = mode == kModeCommit ? 0 : ((2 * tab_entries + 255) & ~size_t(255));
+  // path keys, path Gram, U~ transposes (8 waves x [kPC][16])
+  const size_t kp = mode == kModeVerify ? 0
+                                        : ((size_t(kPC) * kKpRow * 4 + size_t(kPC) * kGpRow * 4 +
+                                            8 * size_t(kPC) * 16 * 4 + 255) & ~size_t(255));
   const size_t stage = size_t(T + 3) * (kCD + 4) * 4;
   const size_t qk = 2 * size_t(s.TR) * kQRow * 2;
-  const size_t cscr = size_t(kPC) * kCD * 4 + 8 * size_t(kPC) * 16 * 4;  // path values + U transposes
   const size_t frags = 2 * size_t(coef_nfrag(NT)) * kFrag + 4 * size_t(NT) * kFrag;
   size_t big = 0;
   if (mode != kModeCommit) {
     big = stage > qk ? stage : qk;
     big = big > frags ? big : frags;
   }
-  if (mode != kModeVerify) big = big > cscr ? big : cscr;
   s.tab = meta;
   s.kp = s.tab + tab;
   s.big = s.kp + kp;
@@ -155,8 +161,10 @@ __device__ __forceinline__ void split_rne8(const float (&x)[8], bf16x8& hi, bf16
   }
 }
 
-// Workgroup barrier that orders LDS accesses only (global loads and stores
-// issued before it stay in flight).
+// Workgroup barrier that orders LDS accesses only: global loads and stores
+// issued before it stay in flight (a full __syncthreads would wait for all
+// of them, which exposes the latency of every load issued ahead of use).  No
+// thread of these kernels reads global memory that another thread writes.
 __device__ __forceinline__ void lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
@@ -178,6 +186,14 @@ __device__ __forceinline__ float bcast(float x) {
     return dpp_f<SRC * 0x55>(x);  // quad_perm [SRC, SRC, SRC, SRC]
   else
     return dpp_f<0x150 + SRC>(x);  // row_newbcast:SRC
+}
+
+// The thread index as a value the compiler cannot see through: addresses
+// derived from it inside the head loop are computed where they are used
+// instead of being hoisted out of the loop and kept in registers across it.
+__device__ __forceinline__ int opaque_i(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
 }
 
 // f(integral_constant<int, I>) for I = 0 .. N-1, unrolled at compile time
@@ -323,14 +339,90 @@ __device__ __forceinline__ uint4 pack_h8(const float (&y)[8], float sc) {
 // register that moves down by one entry per round, so the slot being
 // resolved is always entry 0 of lane rho % NL.  Writes D[t][i] = r c and
 // C'[t][i] = -c into the fragment arrays (the decay a_i of C' is applied to
-// the X~ product) and a_i into s.a.
+// the X~ product) and a_i into s.a.  s.gt[p] = (beta, alpha, G-row start).
 // ---------------------------------------------------------------------------
-template <int NL>
-__device__ __forceinline__ void coef_recurrence(CoefMeta& s, const _Float16* tabQ, const _Float16* tabG,
-                                                unsigned char* cfr, unsigned char* dfr, int nval, int tid) {
-  constexpr int NPR = kCT / NL;  // nodes per round of the node loop
-  const int q = tid % NL;
-  for (int base = 0; base < nval; base += NPR) {
+
+// next path position: the node itself for slot 0, then the ancestors from the
+// deepest up (highest set position bit first)
+__device__ __forceinline__ int next_pos(int rho, int p, uint64_t& lo, uint64_t& hi) {
+  if (rho == 0) return p;
+  const bool useh = hi != 0;
+  const int bit = 63 - __builtin_clzll((useh ? hi : lo) | 1ull);
+  const uint64_t clr = ~(1ull << bit);
+  hi = useh ? (hi & clr) : hi;
+  lo = useh ? lo : (lo & clr);
+  return useh ? 64 + bit : bit;
+}
+
+// 4 lanes per node (depth < 32).  The tables then have fixed rows of kDRow
+// entries per position in reversed depth order: entry 31 - delta of row p
+// holds the product with p's ancestor (or p itself) at depth delta, every
+// other entry is zero.  The pending sum of slot rho2 of a node at depth d
+// (ancestor depth d - rho2) is then entry 31 - d + rho2 of the row: a fixed
+// offset from a per-round base for each of the lane's 8 slots, and slots
+// already resolved (rho2 <= rho) or beyond the root (rho2 > d) read zeros, so
+// the update needs no masking.  One LDS round trip per step.
+constexpr int kDRow = 66;  // 64 entries + 2 of padding (rows 33 banks apart)
+// K pending sums per lane: slots up to 4 K - 1, i.e. trees of depth < 4 K.
+template <int K>
+__device__ __forceinline__ void coef_recurrence4(CoefMeta& s, const _Float16* tabQ, const _Float16* tabG,
+                                                 unsigned char* cfr, unsigned char* dfr, int nval, int tid) {
+  constexpr int NL = 4;
+  const int q = tid & 3;
+  for (int base = 0; base < nval; base += kCT / NL) {
+    const int p = base + tid / NL;
+    const bool active = p < nval;
+    const int d = active ? s.pdep[p] : -1;
+    const int dmax = wave_max_i(d);
+    float w[K];
+    {
+      const _Float16* row = tabQ + (active ? p : 0) * kDRow + 31 - (active ? d : 0) + q;
+#pragma unroll
+      for (int k = 0; k < K; ++k) w[k] = (float)row[4 * k];
+    }
+    uint64_t lo = active ? s.ancp[p][0] : 0, hi = active ? s.ancp[p][1] : 0;
+    float r = 1.0f;
+    for (int rho0 = 0; rho0 <= dmax; rho0 += NL) {
+      // entry of slot rho0 + q in any row (clamped for lanes past their root,
+      // whose reads are not used)
+      int e0 = 31 - d + rho0 + q;
+      e0 = e0 < 35 ? e0 : 35;
+      static_for<NL>([&](auto jc) __attribute__((always_inline)) {
+        constexpr int j = decltype(jc)::value;
+        const int rho = rho0 + j;
+        const bool act = active && rho <= d;
+        const int pos = next_pos(rho, p, lo, hi);
+        const int ps = act ? pos : 0;
+        const float2 gba = *reinterpret_cast<const float2*>(&s.gt[ps]);
+        const _Float16* row = tabG + ps * kDRow + e0;
+        float gv[K];
+#pragma unroll
+        for (int k2 = 0; k2 < K; ++k2) gv[k2] = (float)row[4 * k2];
+        const float c = gba.x * bcast<NL, j>(w[0]);
+        if (act && q == j) {
+          *reinterpret_cast<_Float16*>(dfr + cfrag_off(ps, p)) = (_Float16)(r * c);
+          *reinterpret_cast<_Float16*>(cfr + cfrag_off(ps, p)) = (_Float16)(-c);
+        }
+        r *= act ? gba.y : 1.0f;
+#pragma unroll
+        for (int k2 = 0; k2 < K; ++k2) w[k2] = fmaf(-c, gv[k2], w[k2]);
+        __builtin_amdgcn_sched_barrier(0);  // one step's loads live at a time
+      });
+#pragma unroll
+      for (int k = 0; k < K - 1; ++k) w[k] = w[k + 1];
+      w[K - 1] = 0.0f;
+    }
+    if (active && q == 0) s.a[p] = r;
+  }
+}
+
+// 16 lanes per node (any depth up to 127): the general case, one step at a
+// time with the pending sum broadcast through ds_bpermute.
+__device__ __forceinline__ void coef_recurrence16(CoefMeta& s, const _Float16* tabQ, const _Float16* tabG,
+                                                  unsigned char* cfr, unsigned char* dfr, int nval, int tid) {
+  constexpr int NL = 16;
+  const int q = tid & 15;
+  for (int base = 0; base < nval; base += kCT / NL) {
     const int p = base + tid / NL;
     const bool active = p < nval;
     const int d = active ? s.pdep[p] : -1;
@@ -344,62 +436,267 @@ __device__ __forceinline__ void coef_recurrence(CoefMeta& s, const _Float16* tab
     }
     uint64_t lo = active ? s.ancp[p][0] : 0, hi = active ? s.ancp[p][1] : 0;
     float r = 1.0f;
-    int rho0_ = 0;
-    // one step of the recurrence: slot rho = rho0 + j, whose pending sum
-    // sv was broadcast from entry 0 of lane j of the group
-    auto step = [&](int j, float sv) __attribute__((always_inline)) {
-      const int rho = rho0_ + j;
-      const bool act = active && rho <= d;
-      // position of the path node at slot rho: the node itself, then the
-      // ancestors from the deepest up (highest set position bit first)
-      int pos = p;
-      if (rho > 0) {
-        const bool useh = hi != 0;
-        const int bit = 63 - __builtin_clzll((useh ? hi : lo) | 1ull);
-        pos = useh ? 64 + bit : bit;
-        const uint64_t clr = ~(1ull << bit);
-        hi = useh ? (hi & clr) : hi;
-        lo = useh ? lo : (lo & clr);
-      }
-      const int ps = act ? pos : 0;
-      const float c = s.be[ps] * sv;
-      if (act && q == j) {
-        *reinterpret_cast<_Float16*>(dfr + cfrag_off(ps, p)) = (_Float16)(r * c);
-        *reinterpret_cast<_Float16*>(cfr + cfrag_off(ps, p)) = (_Float16)(-c);
-      }
-      r *= act ? s.al[ps] : 1.0f;
-      const int go = s.qoff[ps] - ps;  // start of the G row of the path node
-      // every table read is issued (index clamped where the entry is not
-      // needed) so that they overlap; the update is masked arithmetically
-      float gv[8];
+    const int gbase = (tid & 63) & ~(NL - 1);
+    for (int rho0 = 0; rho0 <= dmax; rho0 += NL) {
+      for (int j = 0; j < NL; ++j) {
+        const int rho = rho0 + j;
+        const bool act = active && rho <= d;
+        const int pos = next_pos(rho, p, lo, hi);
+        const int ps = act ? pos : 0;
+        const float4 gt = s.gt[ps];
+        const float c = gt.x * __shfl(w[0], gbase + j);
+        if (act && q == j) {
+          *reinterpret_cast<_Float16*>(dfr + cfrag_off(ps, p)) = (_Float16)(r * c);
+          *reinterpret_cast<_Float16*>(cfr + cfrag_off(ps, p)) = (_Float16)(-c);
+        }
+        r *= act ? gt.y : 1.0f;
+        const int go = __float_as_int(gt.z);
+        float gv[8];
 #pragma unroll
-      for (int k2 = 0; k2 < 8; ++k2) {
-        const int rho2 = rho0_ + NL * k2 + q;
-        const bool u = act && rho2 > rho && rho2 <= d;
-        gv[k2] = (float)tabG[u ? go + d - rho2 : 0];
-      }
+        for (int k2 = 0; k2 < 8; ++k2) {
+          const int rho2 = rho0 + NL * k2 + q;
+          const bool u = act && rho2 > rho && rho2 <= d;
+          gv[k2] = (float)tabG[u ? go + d - rho2 : 0];
+        }
 #pragma unroll
-      for (int k2 = 0; k2 < 8; ++k2) {
-        const int rho2 = rho0_ + NL * k2 + q;
-        const bool u = act && rho2 > rho && rho2 <= d;
-        w[k2] = fmaf(u ? -c : 0.0f, gv[k2], w[k2]);
-      }
-    };
-    for (rho0_ = 0; rho0_ <= dmax; rho0_ += NL) {
-      if constexpr (NL == 4) {
-        static_for<4>([&](auto jc) __attribute__((always_inline)) {
-          constexpr int j = decltype(jc)::value;
-          step(j, bcast<4, j>(w[0]));
-        });
-      } else {
-        const int gbase = (tid & 63) & ~(NL - 1);
-        for (int j = 0; j < NL; ++j) step(j, __shfl(w[0], gbase + j));
+        for (int k2 = 0; k2 < 8; ++k2) {
+          const int rho2 = rho0 + NL * k2 + q;
+          const bool u = act && rho2 > rho && rho2 <= d;
+          w[k2] = fmaf(u ? -c : 0.0f, gv[k2], w[k2]);
+        }
       }
 #pragma unroll
       for (int k = 0; k < 7; ++k) w[k] = w[k + 1];
       w[7] = 0.0f;
     }
     if (active && q == 0) s.a[p] = r;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Path-key features of one commit chunk (path slots m0 .. m0 + cnt - 1): conv
+// along the path (conv state before the commit above the root) + SiLU + L2
+// norm -> s_kp (fp32 rows), then the chunk's Gram matrix -> s_gp (bf16x3
+// MFMA on waves 0..3).  Ends with a barrier.
+// ---------------------------------------------------------------------------
+template <typename TIn>
+__device__ __forceinline__ void kp_features(const CoefParams& p, const CoefMeta& s, float* s_kp, float* s_gp,
+                                            int b, int g, int m0, int cnt, int tid) {
+  const int T = p.T, Hk = p.Hk, DK = p.DK;
+  const int C = 2 * Hk * DK + p.Hv * p.DV;
+  const int kch0 = Hk * DK + g * DK;
+  const int cg = tid & 15, j = tid >> 4;  // 8 channels of path slot m0 + j
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+  const TIn* pk = static_cast<const TIn*>(p.pk);
+  float x[4][8], wk[8][4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int mm = m0 + j - 3 + t;
+    if (j < cnt && mm >= 0 && 8 * cg < DK) {
+      load8(pk + (size_t(b) * T + s.ppath[mm]) * Hk * DK + size_t(g) * DK + 8 * cg, x[t]);
+    } else if (j < cnt && mm < 0 && 8 * cg < DK) {
+      load8(p.conv_state + (size_t(b) * 3 + mm + 3) * C + kch0 + 8 * cg, x[t]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[t][e] = 0.0f;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int c = 8 * cg + e;
+    const float4 w4 = c < DK ? *reinterpret_cast<const float4*>(p.conv_w + size_t(kch0 + c) * 4)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+    wk[e][0] = w4.x;
+    wk[e][1] = w4.y;
+    wk[e][2] = w4.z;
+    wk[e][3] = w4.w;
+  }
+  float y[8];
+  float ss = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float v = fmaf(wk[e][3], x[3][e], fmaf(wk[e][2], x[2][e], fmaf(wk[e][1], x[1][e], wk[e][0] * x[0][e])));
+    y[e] = (j < cnt && 8 * cg + e < DK) ? silu(v) : 0.0f;
+    ss = fmaf(y[e], y[e], ss);
+  }
+  ss = group_sum<16>(ss);
+  const float inv = rsqrt_hw(ss + 1e-6f);
+  float* dst = s_kp + j * kKpRow + 8 * cg;
+  *reinterpret_cast<float4*>(dst) = make_float4(y[0] * inv, y[1] * inv, y[2] * inv, y[3] * inv);
+  *reinterpret_cast<float4*>(dst + 4) = make_float4(y[4] * inv, y[5] * inv, y[6] * inv, y[7] * inv);
+  lds_sync();
+  if (wave < 4) {  // path Gram Kp Kp^T (32 x 32)
+    const int ti = wave >> 1, tj = wave & 1;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      float xa[8], xb[8];
+      load8(s_kp + (16 * ti + l16) * kKpRow + 32 * kb + 8 * lg, xa);
+      load8(s_kp + (16 * tj + l16) * kKpRow + 32 * kb + 8 * lg, xb);
+      bf16x8 ah, al, bh, bl;
+      split_rne8(xa, ah, al);
+      split_rne8(xb, bh, bl);
+      acc = mfma3(ah, al, bh, bl, acc);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s_gp[(16 * ti + 4 * lg + i) * kGpRow + 16 * tj + l16] = acc[i];
+  }
+  lds_sync();
+}
+
+// Streaming load of 16 bytes (raw rows, read once): the non-temporal hint
+// keeps them from displacing the state rows in the caches.
+__device__ __forceinline__ uint4 load_stream16(const void* src) {
+  typedef unsigned u32v4 __attribute__((ext_vector_type(4)));
+  const u32v4 v = __builtin_nontemporal_load(reinterpret_cast<const u32v4*>(src));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// ---------------------------------------------------------------------------
+// Inputs of one value head, loaded into registers one head ahead (the
+// loads are issued before the previous head's outputs are stored, so that
+// waiting for them does not wait for those stores) and written to LDS at
+// the head's start.
+// ---------------------------------------------------------------------------
+template <typename TIn>
+struct Raw4T;
+template <>
+struct Raw4T<BF16> {
+  typedef uint2 type;
+};
+template <>
+struct Raw4T<float> {
+  typedef uint4 type;
+};
+__device__ __forceinline__ float4 raw4_f32(const uint2& u) {
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+__device__ __forceinline__ float4 raw4_f32(const uint4& u) {
+  return make_float4(__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w));
+}
+
+template <typename TIn, int MODE>
+struct HeadIn {
+  static constexpr int EPC = 16 / sizeof(TIn);
+  static constexpr int NVC = kCMaxT * kCD / EPC / kCT;  // 16-byte raw-v chunks per thread
+  static constexpr bool kStep = MODE == kModeStep;
+  typedef typename Raw4T<TIn>::type Raw4;
+  uint4 raw[NVC];
+  TIn al, be;   // gates of position tid
+  float wv;     // v conv weight: tap tid / 128, channel tid % 128
+  float cs;     // conv-state slot tid / 128, channel tid % 128 seen by this step
+  float cso;    // the same slot before the commit (path features of the commit)
+  TIn pal, pbe;  // gates of path slot tid
+  Raw4 pt[2][4];  // raw path values: slot 16 u + l16, channels 16 wave + 4 lg .. + 3, tap t
+
+  __device__ __forceinline__ void load(const CoefParams& p, const CoefMeta& s, int b, int h, int Lp, bool vok,
+                                       int tid) {
+    const int T = p.T, Hk = p.Hk, Hv = p.Hv, DK = p.DK, DV = p.DV;
+    const int C = 2 * Hk * DK + Hv * DV;
+    const int vch0 = 2 * Hk * DK + h * DV;
+    const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, lg = lane >> 4;
+    if (vok) {
+      const TIn* src = static_cast<const TIn*>(p.v) + size_t(b) * T * Hv * DV + size_t(h) * DV;
+      const int cpr = DV / EPC;
+#pragma unroll
+      for (int jj = 0; jj < NVC; ++jj) {
+        const int idx = jj * kCT + tid;
+        const int ok = idx < T * cpr;
+        const int r = ok ? idx / cpr : 0, c = ok ? idx % cpr : 0;
+        raw[jj] = load_stream16(src + size_t(s.ord[r]) * Hv * DV + c * EPC);
+      }
+      const size_t ai = (size_t(b) * T + s.ord[tid < T ? tid : 0]) * Hv + h;
+      al = static_cast<const TIn*>(p.alpha)[ai];
+      be = static_cast<const TIn*>(p.beta)[ai];
+      {
+        const int i = tid < 3 * kCD ? tid : 0;
+        const int sl = i / kCD, c = i % kCD;
+        cs = c < DV ? conv_slot<TIn>(p, s, b, kStep ? Lp : 0, sl, vch0 + c, static_cast<const TIn*>(p.pv),
+                                     size_t(Hv) * DV, h * DV + c)
+                    : 0.0f;
+      }
+    }
+    if (vok || (MODE != kModeVerify && Lp > 0)) {  // v conv weights (verify and path values)
+      const int c = tid % kCD, t = tid / kCD;
+      wv = c < DV ? p.conv_w[size_t(vch0 + c) * 4 + t] : 0.0f;
+    }
+    if constexpr (MODE != kModeVerify) {
+      if (Lp > 0) {
+        const int i = tid < 3 * kCD ? tid : 0;
+        const int sl = i / kCD, c = i % kCD;
+        cso = c < DV ? p.conv_state[(size_t(b) * 3 + sl) * C + vch0 + c] : 0.0f;
+        const size_t ai = (size_t(b) * T + s.ppath[tid < Lp ? tid : 0]) * Hv + h;
+        pal = static_cast<const TIn*>(p.palpha)[ai];
+        pbe = static_cast<const TIn*>(p.pbeta)[ai];
+        const int cl = 16 * wave + 4 * lg;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const int mm = 16 * u + l16 - 3 + t;
+            const int node = s.ppath[(mm >= 0 && mm < Lp) ? mm : 0];
+            pt[u][t] = *reinterpret_cast<const Raw4*>(static_cast<const TIn*>(p.pv) +
+                                                      (size_t(b) * T + node) * Hv * DV + size_t(h) * DV +
+                                                      (cl < DV ? cl : 0));
+          }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(const CoefParams& p, CoefMeta& s, float* stage, int Lp, bool vok,
+                                        int tid) const {
+    const int T = p.T, DV = p.DV;
+    if (vok) {
+      const int cpr = DV / EPC;
+#pragma unroll
+      for (int jj = 0; jj < NVC; ++jj) {
+        const int idx = jj * kCT + tid;
+        if (idx < T * cpr) {
+          const int r = idx / cpr, c = idx % cpr;
+          float* to = stage + r * kSRow + c * EPC;
+          if constexpr (sizeof(TIn) == 2) {
+            const uint4 u = raw[jj];
+            *reinterpret_cast<float4*>(to) = raw4_f32(make_uint2(u.x, u.y));
+            *reinterpret_cast<float4*>(to + 4) = raw4_f32(make_uint2(u.z, u.w));
+          } else {
+            *reinterpret_cast<uint4*>(to) = raw[jj];
+          }
+        }
+      }
+      if (tid < 3 * kCD) stage[(T + tid / kCD) * kSRow + tid % kCD] = cs;
+      if (tid < T) {
+        const int go = s.qoff[tid] - tid;
+        s.gt[tid] = make_float4(to_f32(be), to_f32(al), __int_as_float(go), 0.0f);
+      }
+    }
+    if (vok || (MODE != kModeVerify && Lp > 0)) s.wv[tid / kCD][tid % kCD] = wv;
+    if constexpr (MODE != kModeVerify) {
+      if (Lp > 0) {
+        if (tid < 3 * kCD) s.cso[tid / kCD][tid % kCD] = cso;
+        if (tid < Lp) {
+          s.pal[tid] = to_f32(pal);
+          s.pbe[tid] = to_f32(pbe);
+        }
+      }
+    }
+  }
+};
+
+// state rows of head h in the S^T accumulator layout (16 dk columns ...)
+__device__ __forceinline__ void load_state(const float* S, int b, int Hv, int DV, int DK, int h, int wave, int l16,
+                                           int lg, float (&sf)[8][4]) {
+  const float* Sb = S + (size_t(b) * Hv + h) * size_t(DV) * DK;
+  const int dv = 16 * wave + l16;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const int dk = 16 * t + 4 * lg;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (dv < DV && dk < DK) v = *reinterpret_cast<const float4*>(Sb + size_t(dv) * DK + dk);
+    sf[t][0] = v.x;
+    sf[t][1] = v.y;
+    sf[t][2] = v.z;
+    sf[t][3] = v.w;
   }
 }
 
@@ -411,15 +708,19 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
   extern __shared__ __align__(16) unsigned char smem[];
   constexpr bool kVerify = MODE != kModeCommit;
   constexpr bool kCommit = MODE != kModeVerify;
+  constexpr int EPC = 16 / sizeof(TIn);
+  constexpr int NVC = HeadIn<TIn, MODE>::NVC;
   CoefMeta& s = *reinterpret_cast<CoefMeta*>(smem);
   const int T = p.T, Hk = p.Hk, Hv = p.Hv, DK = p.DK, DV = p.DV;
   const CoefSmem L_ = coef_smem(T, MODE, sizeof(TIn));
   const int TR = L_.TR;
   _Float16* tabQ = reinterpret_cast<_Float16*>(smem + L_.tab);
-  _Float16* tabG = tabQ + (T * (T + 1)) / 2;
+  _Float16* tabG = tabQ;  // set once the tree's depth is known
   float* s_kp = reinterpret_cast<float*>(smem + L_.kp);  // [kPC][kKpRow] path keys
   float* s_gp = s_kp + kPC * kKpRow;                      // [kPC][kGpRow] path Gram
+  float* s_ut0 = s_gp + kPC * kGpRow;                     // 8 x [kPC][16] U~ transposes
   unsigned char* big = smem + L_.big;
+  float* stage = reinterpret_cast<float*>(big);
 
   const int G = Hv / Hk;
   const int nhg = G / p.hpw;
@@ -431,7 +732,7 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
   const int l16 = lane & 15, lg = lane >> 4;
   const int NT = (T + 15) / 16;
   const int KBP = (T + 31) / 32;
-  const TIn* vin = static_cast<const TIn*>(p.v);
+
 
   // ---- commit path (step / commit): the accepted node's path, root first
   int Lp = 0;
@@ -468,8 +769,9 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
     }
     if (tid <= T) s.qoff[tid] = m.qoff[size_t(b) * (T + 1) + tid];
   }
-  __syncthreads();
+  lds_sync();
   if constexpr (kVerify) {
+    if (tid >= T && tid < kCMaxT) s.tap[tid] = 0;  // positions past the tree read row 0
     if (tid < T) {  // staged rows of the 4 conv taps of position tid
       const int d = s.pdep[tid];
       const int t2 = s.ppos[tid];
@@ -486,6 +788,11 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
     }
   }
   const bool vok = kVerify && tstat == GDN_TREE_OK;
+  // trees of depth < 32: fixed-row tables and 4 lanes per node in the
+  // recurrence; deeper trees: ragged rows (offsets qoff) and 16 lanes
+  const bool shallow = (nval > 0 ? s.pdep[nval - 1] : 0) < 32;
+  tabG = tabQ + (shallow ? T * kDRow : (T * (T + 1)) / 2);
+
 
   // ---- per key head: Q~, K~, Gram tables, K~^T operand and Q~ init
   h8 kta[4];   // A operand of X~^T: K~^T rows 16 wave + l16, positions 32 kb + 8 lg ..
@@ -495,26 +802,50 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
 #pragma unroll
   for (int nt = 0; nt < 8; ++nt) qin[nt] = h4{0, 0, 0, 0};
   if (vok) {
-    const TIn* qs = static_cast<const TIn*>(p.q) + size_t(b) * T * Hk * DK + size_t(g) * DK;
-    const TIn* ks = static_cast<const TIn*>(p.k) + size_t(b) * T * Hk * DK + size_t(g) * DK;
     const TIn* pqs = static_cast<const TIn*>(p.pq);
     const TIn* pks = static_cast<const TIn*>(p.pk);
     const int cg = tid & 15, nj = tid >> 4;
+    const int cpr = DK / EPC;
+    // raw q and k rows and the conv-state rows of both, issued together
+    uint4 rq[2][NVC];
+    float csq[2];
+#pragma unroll
+    for (int part = 0; part < 2; ++part) {
+      const TIn* src = static_cast<const TIn*>(part ? p.k : p.q) + size_t(b) * T * Hk * DK + size_t(g) * DK;
+#pragma unroll
+      for (int jj = 0; jj < NVC; ++jj) {
+        const int idx = jj * kCT + tid;
+        const int ok = idx < T * cpr;
+        const int r = ok ? idx / cpr : 0, c = ok ? idx % cpr : 0;
+        rq[part][jj] = load_stream16(src + size_t(s.ord[r]) * Hk * DK + c * EPC);
+      }
+      const int i = tid < 3 * kCD ? tid : 0;
+      const int sl = i / kCD, c = i % kCD;
+      csq[part] = c < DK ? conv_slot<TIn>(p, s, b, MODE == kModeStep ? Lp : 0, sl, part * Hk * DK + g * DK + c,
+                                          part ? pks : pqs, size_t(Hk) * DK, g * DK + c)
+                         : 0.0f;
+    }
     uint4 qk_out[2][4];
 #pragma unroll
     for (int part = 0; part < 2; ++part) {
       const int ch0 = part * Hk * DK + g * DK;
-      __syncthreads();  // previous staging consumed
-      float* stage = reinterpret_cast<float*>(big);
-      stage_rows<TIn>(stage, part ? ks : qs, size_t(Hk) * DK, DK, s, T, tid);
-      for (int i = tid; i < 3 * kCD; i += kCT) {
-        const int sl = i / kCD, c = i % kCD;
-        float x = 0.0f;
-        if (c < DK)
-          x = conv_slot<TIn>(p, s, b, MODE == kModeStep ? Lp : 0, sl, ch0 + c, part ? pks : pqs,
-                             size_t(Hk) * DK, g * DK + c);
-        stage[(T + sl) * kSRow + c] = x;
+      if (part) lds_sync();  // q staging consumed
+#pragma unroll
+      for (int jj = 0; jj < NVC; ++jj) {
+        const int idx = jj * kCT + tid;
+        if (idx < T * cpr) {
+          const int r = idx / cpr, c = idx % cpr;
+          float* to = stage + r * kSRow + c * EPC;
+          if constexpr (sizeof(TIn) == 2) {
+            const uint4 u = rq[part][jj];
+            *reinterpret_cast<float4*>(to) = raw4_f32(make_uint2(u.x, u.y));
+            *reinterpret_cast<float4*>(to + 4) = raw4_f32(make_uint2(u.z, u.w));
+          } else {
+            *reinterpret_cast<uint4*>(to) = rq[part][jj];
+          }
+        }
       }
+      if (tid < 3 * kCD) stage[(T + tid / kCD) * kSRow + tid % kCD] = csq[part];
       float wq[8][4];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -526,14 +857,13 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
         wq[e][2] = w4.z;
         wq[e][3] = w4.w;
       }
-      __syncthreads();
+      lds_sync();
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int pos = 32 * r + nj;
         float y[8];
-        const bool real = pos < nval;
-        if (real) {
-          conv8(reinterpret_cast<const float*>(big), s, pos, cg, DK, wq, y);
+        if (pos < nval) {
+          conv8(stage, s, pos, cg, DK, wq, y);
         } else {
 #pragma unroll
           for (int e = 0; e < 8; ++e) y[e] = 0.0f;
@@ -545,7 +875,11 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
         qk_out[part][r] = pack_h8(y, rsqrt_hw(ss + 1e-6f));
       }
     }
-    __syncthreads();  // staging consumed: Q~, K~ rows go to the same region
+    if (shallow) {  // the fixed-row tables are zero outside the entries written below
+      const int n16 = (2 * T * kDRow * 2 + 15) / 16;
+      for (int i = tid; i < n16; i += kCT) reinterpret_cast<uint4*>(tabQ)[i] = make_uint4(0, 0, 0, 0);
+    }
+    lds_sync();  // staging consumed: Q~, K~ rows go to the same region
     _Float16* s_q = reinterpret_cast<_Float16*>(big);
     _Float16* s_k = s_q + TR * kQRow;
 #pragma unroll
@@ -556,7 +890,7 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
         *reinterpret_cast<uint4*>(s_k + pos * kQRow + 8 * cg) = qk_out[1][r];
       }
     }
-    __syncthreads();
+    lds_sync();
     // Gram tiles (pt, pt2), pt2 <= pt: Q K^T (ancestors and self) and K K^T
     // (proper ancestors) scattered into the ragged tables
     const int ntile = NT * (NT + 1) / 2;
@@ -574,14 +908,17 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
         ag = mma16(a2, bk, ag);
       }
       const int pc = 16 * pt2 + l16;
+      const int dc = s.pdep[pc];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int pr = 16 * pt + 4 * lg + i;
         if (pr < nval && pc <= pr) {
           const bool anc = (s.ancp[pr][pc >> 6] >> (pc & 63)) & 1ull;
-          const int dc = s.pdep[pc];
-          if (anc || pc == pr) tabQ[s.qoff[pr] + dc] = (_Float16)aq[i];
-          if (anc) tabG[s.qoff[pr] - pr + dc] = (_Float16)ag[i];
+          // shallow trees: reversed fixed rows; deep trees: ragged rows
+          const int iq = shallow ? pr * kDRow + 31 - dc : s.qoff[pr] + dc;
+          const int ig = shallow ? pr * kDRow + 31 - dc : s.qoff[pr] - pr + dc;
+          if (anc || pc == pr) tabQ[iq] = (_Float16)aq[i];
+          if (anc) tabG[ig] = (_Float16)ag[i];
         }
       }
     }
@@ -598,156 +935,84 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt)
       if (nt < NT) qin[nt] = *reinterpret_cast<const h4*>(s_q + (16 * nt + l16) * kQRow + 16 * wave + 4 * lg);
-    __syncthreads();  // Q~ / K~ tiles consumed
+    lds_sync();  // Q~ / K~ tiles consumed
   }
 
-  // ---- commit features of the path keys (shared by the value heads)
-  int kp_chunk = -1;  // chunk whose key features are in s_kp / s_gp
+  // inputs and state of the first value head
+  HeadIn<TIn, MODE> hin;
+  hin.load(p, s, b, h0, Lp, vok, tid);
+  float sf[8][4];
+  load_state(kCommit ? p.S : p.S0, b, Hv, DV, DK, h0, wave, l16, lg, sf);
+
+  // ---- commit: path-key features of the first chunk (shared by the heads)
   const int nchunks = (Lp + kPC - 1) / kPC;
+  if constexpr (kCommit) {
+    if (Lp > 0) kp_features<TIn>(p, s, s_kp, s_gp, b, g, 0, Lp < kPC ? Lp : kPC, tid);
+  }
 
   // ---- value heads
   for (int hh = 0; hh < p.hpw; ++hh) {
     const int h = h0 + hh;
-    const int vch0 = 2 * Hk * DK + h * DV;
-    // state of this head in the S^T accumulator layout
-    float sf[8][4];
-    {
-      const float* Sb = (kCommit ? p.S : p.S0) + (size_t(b) * Hv + h) * size_t(DV) * DK;
-      const int dv = 16 * wave + l16;
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const int dk = 16 * t + 4 * lg;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (dv < DV && dk < DK) v = *reinterpret_cast<const float4*>(Sb + size_t(dv) * DK + dk);
-        sf[t][0] = v.x;
-        sf[t][1] = v.y;
-        sf[t][2] = v.z;
-        sf[t][3] = v.w;
-      }
-    }
+    const bool more = hh + 1 < p.hpw;
+    // per-lane indices re-derived inside the loop (see opaque_i)
+    const int tid = opaque_i(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, lg = lane >> 4;
+    // this head's inputs -> LDS (staged raw v + conv rows, gates, weights)
+    hin.store(p, s, stage, Lp, vok, tid);
+    lds_sync();
+
     // ---- commit of the previous accepted path into sf (step / commit)
     if constexpr (kCommit) {
       if (Lp > 0) {
-        const TIn* pk = static_cast<const TIn*>(p.pk);
-        const TIn* pv = static_cast<const TIn*>(p.pv);
-        float* s_vp = reinterpret_cast<float*>(big);           // [kPC][kCD] path values
-        float* s_ut = s_vp + kPC * kCD + wave * (kPC * 16);   // [kPC][16] U transpose of this wave
-        if (tid < Lp) {
-          const size_t ai = (size_t(b) * T + s.ppath[tid]) * Hv + h;
-          s.pal[tid] = to_f32(static_cast<const TIn*>(p.palpha)[ai]);
-          s.pbe[tid] = to_f32(static_cast<const TIn*>(p.pbeta)[ai]);
-        }
         for (int ch = 0; ch < nchunks; ++ch) {
+          const int tid = opaque_i(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+          const int l16 = lane & 15, lg = lane >> 4;
+          float* s_ut = s_ut0 + wave * (kPC * 16);  // this wave's U~^T scratch [slot][16]
+          const int cl = 16 * wave + 4 * lg;        // value channels of this lane's rows
           const int m0 = ch * kPC;
           const int cnt = Lp - m0 < kPC ? Lp - m0 : kPC;
-          const int cg = tid & 15, j = tid >> 4;  // 8 channels of path slot m0 + j
-          if (kp_chunk != ch) {
-            // key features of the chunk: conv along the path (old conv state
-            // above the root) + SiLU + L2 norm
-            const int kch0 = Hk * DK + g * DK;
-            float y[8];
+          if (ch > 0) kp_features<TIn>(p, s, s_kp, s_gp, b, g, m0, cnt, tid);
+          // path values of the chunk in the P accumulator layout: slot
+          // 16 u + l16, channels cl .. cl + 3 (conv along the path + SiLU)
+          float vp[2][4];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) y[e] = 0.0f;
-            if (j < cnt) {
+          for (int u = 0; u < 2; ++u) {
+            float4 x[4];
 #pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                const int mm = m0 + j - 3 + t;
-                float x[8];
-                if (mm >= 0) {
-                  if (8 * cg < DK) {
-                    load8(pk + (size_t(b) * T + s.ppath[mm]) * Hk * DK + size_t(g) * DK + 8 * cg, x);
-                  } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) x[e] = 0.0f;
-                  }
+            for (int t = 0; t < 4; ++t) {
+              const int mm = m0 + 16 * u + l16 - 3 + t;
+              if (mm >= 0) {
+                if (ch == 0) {
+                  x[t] = raw4_f32(hin.pt[u][t]);
                 } else {
-#pragma unroll
-                  for (int e = 0; e < 8; ++e)
-                    x[e] = 8 * cg + e < DK ? p.conv_state[(size_t(b) * 3 + mm + 3) * C + kch0 + 8 * cg + e] : 0.0f;
+                  const int node = s.ppath[mm < Lp ? mm : 0];
+                  x[t] = raw4_f32(*reinterpret_cast<const typename Raw4T<TIn>::type*>(
+                      static_cast<const TIn*>(p.pv) + (size_t(b) * T + node) * Hv * DV + size_t(h) * DV +
+                      (cl < DV ? cl : 0)));
                 }
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const int cc = 8 * cg + e;
-                  const float wt = cc < DK ? p.conv_w[size_t(kch0 + cc) * 4 + t] : 0.0f;
-                  y[e] = fmaf(wt, x[e], y[e]);
-                }
+              } else {
+                x[t] = *reinterpret_cast<const float4*>(&s.cso[mm + 3][cl]);
               }
-#pragma unroll
-              for (int e = 0; e < 8; ++e) y[e] = 8 * cg + e < DK ? silu(y[e]) : 0.0f;
             }
-            float ss = 0.0f;
+            const bool okv = m0 + 16 * u + l16 < Lp && cl < DV;
+            const float* xs = reinterpret_cast<const float*>(x);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) ss = fmaf(y[e], y[e], ss);
-            ss = group_sum<16>(ss);
-            const float inv = rsqrt_hw(ss + 1e-6f);
-            float* dst = s_kp + j * kKpRow + 8 * cg;
-            *reinterpret_cast<float4*>(dst) = make_float4(y[0] * inv, y[1] * inv, y[2] * inv, y[3] * inv);
-            *reinterpret_cast<float4*>(dst + 4) = make_float4(y[4] * inv, y[5] * inv, y[6] * inv, y[7] * inv);
-            __syncthreads();
-            // path Gram Kp Kp^T (32 x 32), bf16x3 on waves 0..3
-            if (wave < 4) {
-              const int ti = wave >> 1, tj = wave & 1;
-              f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-              for (int kb = 0; kb < 4; ++kb) {
-                float xa[8], xb[8];
-                load8(s_kp + (16 * ti + l16) * kKpRow + 32 * kb + 8 * lg, xa);
-                load8(s_kp + (16 * tj + l16) * kKpRow + 32 * kb + 8 * lg, xb);
-                bf16x8 ah, al, bh, bl;
-                split_rne8(xa, ah, al);
-                split_rne8(xb, bh, bl);
-                acc = mfma3(ah, al, bh, bl, acc);
-              }
-#pragma unroll
-              for (int i = 0; i < 4; ++i) s_gp[(16 * ti + 4 * lg + i) * kGpRow + 16 * tj + l16] = acc[i];
+            for (int i = 0; i < 4; ++i) {
+              const float y = fmaf(s.wv[3][cl + i], xs[12 + i],
+                                   fmaf(s.wv[2][cl + i], xs[8 + i],
+                                        fmaf(s.wv[1][cl + i], xs[4 + i], s.wv[0][cl + i] * xs[i])));
+              vp[u][i] = okv ? silu(y) : 0.0f;
             }
-            kp_chunk = ch;
-          }
-          // value features of the chunk for this head (conv + SiLU, no norm)
-          {
-            float y[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) y[e] = 0.0f;
-            if (j < cnt) {
-#pragma unroll
-              for (int t = 0; t < 4; ++t) {
-                const int mm = m0 + j - 3 + t;
-                float x[8];
-                if (mm >= 0) {
-                  if (8 * cg < DV) {
-                    load8(pv + (size_t(b) * T + s.ppath[mm]) * Hv * DV + size_t(h) * DV + 8 * cg, x);
-                  } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) x[e] = 0.0f;
-                  }
-                } else {
-#pragma unroll
-                  for (int e = 0; e < 8; ++e)
-                    x[e] = 8 * cg + e < DV ? p.conv_state[(size_t(b) * 3 + mm + 3) * C + vch0 + 8 * cg + e] : 0.0f;
-                }
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const int cc = 8 * cg + e;
-                  const float wt = cc < DV ? p.conv_w[size_t(vch0 + cc) * 4 + t] : 0.0f;
-                  y[e] = fmaf(wt, x[e], y[e]);
-                }
-              }
-#pragma unroll
-              for (int e = 0; e < 8; ++e) y[e] = 8 * cg + e < DV ? silu(y[e]) : 0.0f;
-            }
-            float* dst = s_vp + j * kCD + 8 * cg;
-            *reinterpret_cast<float4*>(dst) = make_float4(y[0], y[1], y[2], y[3]);
-            *reinterpret_cast<float4*>(dst + 4) = make_float4(y[4], y[5], y[6], y[7]);
           }
           if (tid < kPC) {  // alpha products after slot m0 + tid within the chunk
             float sp = 1.0f;
             for (int m = tid + 1; m < cnt; ++m) sp *= s.pal[m0 + m];
             s.psuf[m0 + tid] = tid < cnt ? sp : 0.0f;
           }
-          __syncthreads();
+          lds_sync();
           float Ac = 1.0f;  // alpha product over the chunk
           for (int m = 0; m < cnt; ++m) Ac *= s.pal[m0 + m];
-          // P = S Kp^T (rows 16 wave + 4 lg + i, path slot 16 u + l16)
+          // P = S Kp^T (rows cl + i, path slot 16 u + l16)
           f32x4 P[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
           for (int kb = 0; kb < 4; ++kb) {
@@ -767,10 +1032,9 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
             }
           }
           // recurrence over the chunk's path nodes: u_j = beta_j (v_j - alpha_j T_j),
-          // T_m <- alpha_j T_m + u_j (k_j . k_m) for the later slots m
+          // T_m <- alpha_j T_m + u_j (k_j . k_m) for the later slots m; T_j and v_j
+          // of this lane group's rows are in lane j of tile j / 16 (row broadcast)
           f32x4 U[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-          // slots 16 ut + j: T_j of the 16 rows of this lane group is in lane j
-          // of tile ut (row broadcast); the later slots are in tiles >= ut
           static_for<2>([&](auto utc) __attribute__((always_inline)) {
             constexpr int ut = decltype(utc)::value;
             if (16 * ut >= cnt) return;
@@ -778,13 +1042,11 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
               constexpr int j = decltype(jc)::value;
               const int jj = 16 * ut + j;
               if (jj >= cnt) return;
-              float tj[4];
-#pragma unroll
-              for (int i = 0; i < 4; ++i) tj[i] = bcast<16, j>(P[ut][i]);
-              const float4 v4 = *reinterpret_cast<const float4*>(s_vp + jj * kCD + 16 * wave + 4 * lg);
               const float aj = s.pal[m0 + jj], bj = s.pbe[m0 + jj];
-              const float uj[4] = {bj * (v4.x - aj * tj[0]), bj * (v4.y - aj * tj[1]), bj * (v4.z - aj * tj[2]),
-                                   bj * (v4.w - aj * tj[3])};
+              float uj[4];
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                uj[i] = bj * (bcast<16, j>(vp[ut][i]) - aj * bcast<16, j>(P[ut][i]));
               const bool own = l16 == j;
 #pragma unroll
               for (int i = 0; i < 4; ++i) U[ut][i] = own ? uj[i] : U[ut][i];
@@ -800,7 +1062,7 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
             });
           });
           // u~_m = u_m times the alpha product of the later slots of the chunk;
-          // U^T through this wave's scratch: row slot, 16 value rows
+          // U~^T through this wave's scratch: row slot, 16 value rows
 #pragma unroll
           for (int u = 0; u < 2; ++u) {
             const float f = s.psuf[m0 + 16 * u + l16];
@@ -831,8 +1093,7 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
             sf[t][3] = acc[3];
             __builtin_amdgcn_sched_barrier(0);
           }
-          __syncthreads();  // chunk features consumed
-          if (nchunks > 1) kp_chunk = -1;
+          if (nchunks > 1) lds_sync();  // chunk features consumed before the next chunk's
         }
         // the committed state
         float* Sb = p.S + (size_t(b) * Hv + h) * size_t(DV) * DK;
@@ -846,92 +1107,83 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
       }
     }
 
-    float vt[4][8];  // SiLU(conv v) at channel 16 wave + l16, positions 32 kb + 8 lg + e
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) vt[kb][e] = 0.0f;
-    if (vok) {
-      // stage raw v of this head, gates by position, v conv weights and the
-      // conv-state rows (after the commit in the fused step)
-      float* stage = reinterpret_cast<float*>(big);
-      stage_rows<TIn>(stage, vin + size_t(b) * T * Hv * DV + size_t(h) * DV, size_t(Hv) * DV, DV, s, T, tid);
-      if (tid < T) {
-        const size_t ai = (size_t(b) * T + s.ord[tid]) * Hv + h;
-        s.al[tid] = to_f32(static_cast<const TIn*>(p.alpha)[ai]);
-        s.be[tid] = to_f32(static_cast<const TIn*>(p.beta)[ai]);
+    if (!vok) {
+      if constexpr (kVerify) {  // invalid tree: zero outputs for this head
+        for (int i = tid; i < T * DV / 4; i += kCT) {
+          const int node = i / (DV / 4), c4 = i % (DV / 4);
+          *reinterpret_cast<float4*>(p.out + (size_t(b) * T + node) * size_t(Hv) * DV + size_t(h) * DV + 4 * c4) =
+              make_float4(0.f, 0.f, 0.f, 0.f);
+        }
       }
-      {
-        const int i = tid;  // 4 taps x 128 channels
-        const int tp = i / kCD, c = i % kCD;
-        s.wv[tp][c] = c < DV ? p.conv_w[size_t(vch0 + c) * 4 + tp] : 0.0f;
+      if (more) {
+        lds_sync();  // this head's path tables consumed
+        hin.load(p, s, b, h + 1, Lp, vok, tid);
+        load_state(kCommit ? p.S : p.S0, b, Hv, DV, DK, h + 1, wave, l16, lg, sf);
       }
-      for (int i = tid; i < 3 * kCD; i += kCT) {
-        const int sl = i / kCD, c = i % kCD;
-        stage[(T + sl) * kSRow + c] = c < DV ? conv_slot<TIn>(p, s, b, MODE == kModeStep ? Lp : 0, sl, vch0 + c,
-                                                               static_cast<const TIn*>(p.pv), size_t(Hv) * DV,
-                                                               h * DV + c)
-                                              : 0.0f;
-      }
-      __syncthreads();
-      // v conv in the MFMA operand layout: channel 16 wave + l16
+      continue;
+    }
+
+    // ---- v conv in the MFMA operand layout: channel 16 wave + l16,
+    //      positions 32 kb + 8 lg + e; fp16 with a power-of-two scale per channel
+    h8 va[4];
+    {
       const int c = 16 * wave + l16;
       const float w0 = s.wv[0][c], w1 = s.wv[1][c], w2 = s.wv[2][c], w3 = s.wv[3][c];
+      float vt[4][8];
+      float mx = 0.0f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         if (kb < KBP) {
+          // the taps of 8 consecutive positions, then all 32 staged values
+          const uint4 ta = *reinterpret_cast<const uint4*>(&s.tap[32 * kb + 8 * lg]);
+          const uint4 tb = *reinterpret_cast<const uint4*>(&s.tap[32 * kb + 8 * lg + 4]);
+          const uint32_t taps[8] = {ta.x, ta.y, ta.z, ta.w, tb.x, tb.y, tb.z, tb.w};
+          float x[8][4];
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) x[e][t] = stage[((taps[e] >> (8 * t)) & 255) * kSRow + c];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int pos = 32 * kb + 8 * lg + e;
-            float y = 0.0f;
-            if (pos < nval && c < DV) {
-              const uint32_t taps = s.tap[pos];
-              float x[4];
-#pragma unroll
-              for (int t = 0; t < 4; ++t) x[t] = stage[((taps >> (8 * t)) & 255) * kSRow + c];
-              y = silu(fmaf(w3, x[3], fmaf(w2, x[2], fmaf(w1, x[1], w0 * x[0]))));
-            }
-            vt[kb][e] = y;
+            const float y = silu(fmaf(w3, x[e][3], fmaf(w2, x[e][2], fmaf(w1, x[e][1], w0 * x[e][0]))));
+            vt[kb][e] = (pos < nval && c < DV) ? y : 0.0f;
+            mx = fmaxf(mx, fabsf(vt[kb][e]));
           }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) vt[kb][e] = 0.0f;
         }
       }
-      __syncthreads();  // staging consumed
-    } else if (kVerify) {
-      // invalid tree: zero outputs for this head
-      for (int i = tid; i < T * DV / 4; i += kCT) {
-        const int node = i / (DV / 4), c4 = i % (DV / 4);
-        *reinterpret_cast<float4*>(p.out + (size_t(b) * T + node) * size_t(Hv) * DV + size_t(h) * DV + 4 * c4) =
-            make_float4(0.f, 0.f, 0.f, 0.f);
-      }
+      mx = hmax4(mx);
+      float sc, inv;
+      pow2_scale(mx, sc, inv);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) va[kb][e] = (_Float16)(vt[kb][e] * sc);
+      if (lg == 0) s.rsv[c] = inv;
     }
+    lds_sync();  // staging consumed
 
-    if (!vok) continue;
-
-    // ---- row scales; fp16 operands of the output product
-    h8 sa[4], va[4];
+    // ---- state rows -> fp16 operand with a power-of-two scale per row
+    h8 sa[4];
     {
       float mx = 0.0f;
 #pragma unroll
       for (int t = 0; t < 8; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) mx = fmaxf(mx, fabsf(sf[t][i]));
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(vt[kb][e]));
       mx = hmax4(mx);
       float sc, inv;
       pow2_scale(mx, sc, inv);
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           sa[kb][i] = (_Float16)(sf[2 * kb][i] * sc);
           sa[kb][4 + i] = (_Float16)(sf[2 * kb + 1][i] * sc);
         }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) va[kb][e] = (_Float16)(vt[kb][e] * sc);
-      }
       if (lg == 0) s.rs[16 * wave + l16] = inv;
     }
 
@@ -942,15 +1194,26 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
     for (int i = tid; i < 2 * coef_nfrag(NT) * (kFrag / 16); i += kCT)
       reinterpret_cast<uint4*>(cfr)[i] = make_uint4(0, 0, 0, 0);
     if (tid < kCMaxT) s.a[tid] = 0.0f;
-    __syncthreads();
+    lds_sync();
+    // the next head's inputs and state load during the recurrence (LDS and
+    // VALU bound, the memory pipe is otherwise idle), ahead of this head's
+    // output stores
+    if (more) {
+      hin.load(p, s, b, h + 1, Lp, vok, tid);
+      load_state(kCommit ? p.S : p.S0, b, Hv, DV, DK, h + 1, wave, l16, lg, sf);
+    }
     {
       const int dmax = nval > 0 ? s.pdep[nval - 1] : 0;
-      if (dmax < 32)
-        coef_recurrence<4>(s, tabQ, tabG, cfr, dfr, nval, tid);
+      if (dmax < 12)
+        coef_recurrence4<3>(s, tabQ, tabG, cfr, dfr, nval, tid);
+      else if (dmax < 20)
+        coef_recurrence4<5>(s, tabQ, tabG, cfr, dfr, nval, tid);
+      else if (shallow)
+        coef_recurrence4<8>(s, tabQ, tabG, cfr, dfr, nval, tid);
       else
-        coef_recurrence<16>(s, tabQ, tabG, cfr, dfr, nval, tid);
+        coef_recurrence16(s, tabQ, tabG, cfr, dfr, nval, tid);
     }
-    __syncthreads();
+    lds_sync();
 
     // ---- X~^T = a (Q~^T - K~^T C^T)  (rows: key channels of this wave)
 #pragma unroll
@@ -970,40 +1233,43 @@ __global__ __launch_bounds__(kCT) void coef_kernel(CoefParams p) {
       for (int i = 0; i < 4; ++i) hx[i] = (_Float16)(an * acc[i]);
       *reinterpret_cast<h4*>(xfr + ((wave >> 1) * NT + nt) * kFrag + lane * 16 + (wave & 1) * 8) = hx;
     }
-    __syncthreads();
+    lds_sync();
 
     // ---- O^T = S X~^T + V~^T D^T  (rows: value channels of this wave)
     {
-      const float4 inv4 = *reinterpret_cast<const float4*>(&s.rs[16 * wave + 4 * lg]);
+      const float4 is4 = *reinterpret_cast<const float4*>(&s.rs[16 * wave + 4 * lg]);
+      const float4 iv4 = *reinterpret_cast<const float4*>(&s.rsv[16 * wave + 4 * lg]);
       const int dvr = 16 * wave + 4 * lg;
 #pragma unroll
       for (int nt = 0; nt < 8; ++nt) {
         if (nt >= NT) break;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        f32x4 accs = {0.f, 0.f, 0.f, 0.f}, accv = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
           const h8 bx = *reinterpret_cast<const h8*>(xfr + (kb * NT + nt) * kFrag + lane * 16);
-          acc = mma16(sa[kb], bx, acc);
+          accs = mma16(sa[kb], bx, accs);
         }
         const int base = coef_nfrag(nt);
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
           if (kb > nt / 2) break;
           const h8 bd = *reinterpret_cast<const h8*>(dfr + (base + kb) * kFrag + lane * 16);
-          acc = mma16(va[kb], bd, acc);
+          accv = mma16(va[kb], bd, accv);
         }
         const int pp = 16 * nt + l16;
         if (pp < T && dvr < DV) {
           const int node = s.ord[pp];
           float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
           if (pp < nval)
-            o = make_float4(p.scale * inv4.x * acc[0], p.scale * inv4.y * acc[1], p.scale * inv4.z * acc[2],
-                            p.scale * inv4.w * acc[3]);
+            o = make_float4(p.scale * fmaf(accs[0], is4.x, accv[0] * iv4.x),
+                            p.scale * fmaf(accs[1], is4.y, accv[1] * iv4.y),
+                            p.scale * fmaf(accs[2], is4.z, accv[2] * iv4.z),
+                            p.scale * fmaf(accs[3], is4.w, accv[3] * iv4.w));
           *reinterpret_cast<float4*>(p.out + (size_t(b) * T + node) * size_t(Hv) * DV + size_t(h) * DV + dvr) = o;
         }
       }
     }
-    __syncthreads();  // fragment tiles consumed before the next head
+    lds_sync();  // fragment tiles consumed before the next head
   }
 
   // ---- fused step: conv state after the commit for this workgroup's channels
