@@ -37,7 +37,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-VERIFY_SOURCES = ("paper_2607_06763_amd/csrc/gdn_coef.hip", "paper_2607_06763_amd/csrc/gdn_internal.h")
+VERIFY_SOURCES = ("paper_2607_06763_amd/csrc/gdn_verify.hip", "paper_2607_06763_amd/csrc/gdn_internal.h")
 PROFILES = os.path.join(ROOT, "profiles")
 
 

@@ -90,7 +90,7 @@ int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const
   a.conv_state = conv_state;
   a.S0 = S0;
   a.out = out;
-  return launch_coef_verify(a, stream);
+  return launch_verify(a, stream);
 }
 
 int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* q, const void* k,
@@ -203,7 +203,7 @@ int gdn_tree_step(const gdn_dims* dims, const void* prev_meta, const int32_t* pr
   a.conv_state_out = conv_state_out;
   a.S = S;
   a.commit_status = commit_status;
-  return launch_coef_verify(a, stream);
+  return launch_verify(a, stream);
 }
 
 const char* gdn_last_error(void) { return g_err; }

@@ -22,7 +22,7 @@ constexpr int kRoot = -1;  // parent value of the root
 // a 16-byte aligned offset.
 // ---------------------------------------------------------------------------
 struct MetaLayout {
-  size_t anc, depth, order, pos, parent, status, nvalid, pdep, ppos, ancp, qoff, total;
+  size_t anc, depth, order, pos, parent, status, nvalid, pdep, ppos, total;
   int W;
 };
 
@@ -41,9 +41,7 @@ __host__ __device__ inline MetaLayout meta_layout(int B, int T) {
   m.nvalid = align16(m.status + 4 * size_t(B));
   m.pdep = align16(m.nvalid + 4 * size_t(B));
   m.ppos = align16(m.pdep + 4 * bt);
-  m.ancp = align16(m.ppos + 4 * bt);
-  m.qoff = align16(m.ancp + 8 * bt * m.W);
-  size_t end = m.qoff + 4 * (bt + size_t(B));
+  size_t end = m.ppos + 4 * bt;
   m.total = (end + 255) & ~size_t(255);
   return m;
 }
@@ -58,8 +56,6 @@ struct MetaPtrs {
   int32_t* nvalid;
   int32_t* pdep;
   int32_t* ppos;
-  uint64_t* ancp;
-  int32_t* qoff;
   int W;
 };
 
@@ -76,8 +72,6 @@ __host__ __device__ inline MetaPtrs meta_ptrs(const void* base, int B, int T) {
   m.nvalid = (int32_t*)(p + l.nvalid);
   m.pdep = (int32_t*)(p + l.pdep);
   m.ppos = (int32_t*)(p + l.ppos);
-  m.ancp = (uint64_t*)(p + l.ancp);
-  m.qoff = (int32_t*)(p + l.qoff);
   m.W = l.W;
   return m;
 }
@@ -186,6 +180,103 @@ __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const
 }
 
 // ---------------------------------------------------------------------------
+// Commit building blocks shared by the commit kernel and the fused step.
+// ---------------------------------------------------------------------------
+constexpr int kMC = 32;  // path nodes featurised per chunk
+
+// Inputs of one commit feature task: one conv channel over NW consecutive
+// path nodes m0 .. m0 + NW - 1 (the width-4 conv reaches back to m0 - 3;
+// positions above the root read the conv-state slots).  Every load is
+// unconditional (indices clamped) so that nothing waits for it before the
+// features are computed; the conv-state / padding choice is made when the
+// window is used.
+template <typename TIn, int NW>
+struct FeatWindow {
+  static constexpr int kWin = NW + 3;
+  TIn xr[kWin];  // raw inputs of path nodes m0 - 3 .. m0 + NW - 1 (clamped)
+  float xc[3];   // conv-state slots 0..2 of the channel
+  float4 w;      // conv weights of the channel
+  __device__ __forceinline__ void load(const TIn* src, size_t stride, const float* cs, size_t cstride,
+                                       const float* wrow, const int* s_path, int m0, int L) {
+#pragma unroll
+    for (int q = 0; q < kWin; ++q) {
+      int mi = m0 - 3 + q;
+      mi = mi < 0 ? 0 : (mi < L ? mi : L - 1);
+      xr[q] = src[size_t(s_path[mi]) * stride];
+    }
+#pragma unroll
+    for (int sl = 0; sl < 3; ++sl) xc[sl] = cs[size_t(sl) * cstride];
+    w = *reinterpret_cast<const float4*>(wrow);
+  }
+  // input of the window element q (path node m0 - 3 + q); the conv-state
+  // slot is picked by selects, not by indexing (keeps xc in registers)
+  __device__ __forceinline__ float x(int q, int m0, int L) const {
+    const int mi = m0 - 3 + q;
+    const float c = mi == -3 ? xc[0] : (mi == -2 ? xc[1] : xc[2]);
+    return mi < 0 ? c : (mi < L ? to_f32(xr[q]) : 0.0f);
+  }
+};
+
+
+// One rank-1 step of the commit replay, Eq. 7 in the stored orientation,
+//   S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T,
+// on a thread's pieces of R state rows (CPT consecutive columns each, LPR
+// lanes per row; element i CPT + e is column e of piece i).  The rows are
+// kept as S = gamma * stored (gamma: running product of alpha), so a step is
+// two FMAs per element; kk is the thread's slice of the raw key, inv =
+// 1 / ||k|| is folded into the scalars and vr[i] is v of row piece i.  The
+// R rows share the key slice, which halves the LDS reads per element for
+// R = 2.  Returns the new gamma.
+template <int R, int CPT, int LPR>
+__device__ __forceinline__ float replay_rows(float (&sr)[R * CPT], const float (&kk)[CPT], const float (&vr)[R],
+                                            float al, float be, float inv, float gamma) {
+  float uu[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    float u[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) u[e & 3] += sr[i * CPT + e] * kk[e];
+    uu[i] = (u[0] + u[1]) + (u[2] + u[3]);
+  }
+#pragma unroll
+  for (int i = 0; i < R; ++i) uu[i] = group_sum<LPR>(uu[i]) * inv;  // S_stored . k_hat
+  // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
+  // multiplied by 1 / ||k|| so that it applies to the raw key
+  const float ag = al * gamma;
+  const float ri = __builtin_amdgcn_rcpf(ag) * inv;
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const float c = be * (vr[i] - ag * uu[i]) * ri;
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) sr[i * CPT + e] += c * kk[e];
+  }
+  if (ag < 0x1p-60f) {  // keep the stored frame in range (uniform branch)
+#pragma unroll
+    for (int e = 0; e < R * CPT; ++e) sr[e] *= ag;
+    return 1.0f;
+  }
+  return ag;
+}
+
+// CPT floats of an LDS row (16-byte pieces when CPT % 4 == 0)
+template <int CPT>
+__device__ __forceinline__ void ld_slice(const float* src, float (&x)[CPT]) {
+  if constexpr (CPT % 4 == 0) {
+#pragma unroll
+    for (int e = 0; e < CPT; e += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(src + e);
+      x[e] = v.x;
+      x[e + 1] = v.y;
+      x[e + 2] = v.z;
+      x[e + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) x[e] = src[e];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Launchers (defined in the kernel sources).  All return a gdn_status value.
 // ---------------------------------------------------------------------------
 int launch_prepare(int B, int T, const int32_t* parent, void* meta, int32_t* tree_status,
@@ -207,6 +298,7 @@ struct VerifyArgs {
   float* S = nullptr;
   int32_t* commit_status = nullptr;
 };
+int launch_verify(const VerifyArgs& a, hipStream_t stream);
 // the paper's chunked form (Eq. 9-13) of the same verification
 int launch_verify_chunked(const VerifyArgs& a, hipStream_t stream);
 
@@ -221,11 +313,6 @@ struct CommitArgs {
   int32_t* commit_status;
 };
 int launch_commit(const CommitArgs& a, hipStream_t stream);
-
-// verification / fused step (VerifyArgs.fused) and the state part of the
-// commit on MFMA (gdn_coef.hip)
-int launch_coef_verify(const VerifyArgs& a, hipStream_t stream);
-int launch_coef_commit(const CommitArgs& a, hipStream_t stream);
 
 // Records a message for gdn_last_error() and returns code.
 int set_error(int code, const char* fmt, ...);

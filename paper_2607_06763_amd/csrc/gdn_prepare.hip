@@ -100,12 +100,9 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
       m.parent[base + i] = p;
       m.pdep[base + i] = -1;
       m.ppos[base + i] = -1;
-      m.qoff[size_t(b) * (T + 1) + i] = 0;
       for (int w = 0; w < W; ++w) m.anc[(size_t(base) + i) * W + w] = 0;
-      for (int w = 0; w < W; ++w) m.ancp[(size_t(base) + i) * W + w] = 0;
     }
     if (i == 0) {
-      m.qoff[size_t(b) * (T + 1) + T] = 0;
       m.status[b] = status;
       m.nvalid[b] = 0;
       if (tree_status) tree_status[b] = status;
@@ -138,49 +135,10 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
     s_nxt[i] = rank;  // position of slot i (s_nxt is free after the jumps)
   }
   __syncthreads();
-  if (slot) {  // per-position copies: depth, parent position, ancestor set
+  if (slot) {  // per-position copies: depth and parent position
     const int rank = s_nxt[i];
     m.pdep[base + rank] = real ? dep : -1;
     m.ppos[base + rank] = (real && p >= 0) ? s_nxt[p] : -1;
-    // the proper-ancestor set in position space: bit pos(j) for every
-    // ancestor slot j (positions are sorted by depth, so the set bits in
-    // increasing order are the ancestors from the root down)
-    uint64_t ap[kPrepMaxW];
-#pragma unroll
-    for (int w = 0; w < kPrepMaxW; ++w) ap[w] = 0;
-    for (int w = 0; w < W; ++w) {
-      uint64_t word = real ? anc[w] : 0;
-      while (word) {
-        const int j = 64 * w + __builtin_ctzll(word);
-        word &= word - 1;
-        const int pj = s_nxt[j];
-#pragma unroll
-        for (int w2 = 0; w2 < kPrepMaxW; ++w2)
-          if ((pj >> 6) == w2) ap[w2] |= 1ull << (pj & 63);
-      }
-    }
-    for (int w = 0; w < W; ++w) m.ancp[(size_t(base) + rank) * W + w] = ap[w];
-    s_dep[rank] = real ? dep + 1 : 0;  // (depth + 1) by position; 0 for padding
-  }
-  __syncthreads();
-  // qoff[p] = sum over positions p' < p of (depth + 1): start of the
-  // position's row in the ragged per-ancestor tables of the verify kernel
-  {
-    // thread i sums the entries below i; thread 0 also forms the total
-    // (entry T), since there may be no thread T
-    const int lim = slot ? i : 0;
-    int acc = 0, j = 0;
-    for (; j + 4 <= lim; j += 4) {
-      const int4 k4 = *reinterpret_cast<const int4*>(s_dep + j);
-      acc += (k4.x + k4.y) + (k4.z + k4.w);
-    }
-    for (; j < lim; ++j) acc += s_dep[j];
-    if (slot) m.qoff[size_t(b) * (T + 1) + i] = acc;
-    if (i == 0) {
-      int tot = 0;
-      for (int t = 0; t < T; ++t) tot += s_dep[t];
-      m.qoff[size_t(b) * (T + 1) + T] = tot;
-    }
   }
   if (i == 0) {
     m.status[b] = GDN_TREE_OK;

@@ -271,8 +271,6 @@ def meta_layout(B: int, T: int) -> dict:
     off["nvalid"] = a16(off["status"] + 4 * B)
     off["pdep"] = a16(off["nvalid"] + 4 * B)
     off["ppos"] = a16(off["pdep"] + 4 * B * T)
-    off["ancp"] = a16(off["ppos"] + 4 * B * T)
-    off["qoff"] = a16(off["ancp"] + 8 * B * T * W)
     off["W"] = W
     return off
 
@@ -292,6 +290,4 @@ def unpack_meta(raw, B: int, T: int) -> dict:
                 status=arr("status", np.int32, B, (B,)),
                 nvalid=arr("nvalid", np.int32, B, (B,)),
                 pdep=arr("pdep", np.int32, B * T, (B, T)),
-                ppos=arr("ppos", np.int32, B * T, (B, T)),
-                ancp=arr("ancp", np.uint64, B * T * W, (B, T, W)),
-                qoff=arr("qoff", np.int32, B * (T + 1), (B, T + 1)))
+                ppos=arr("ppos", np.int32, B * T, (B, T)))

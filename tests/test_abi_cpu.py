@@ -46,12 +46,10 @@ def test_meta_bytes_layout(L):
     assert G.meta_bytes(0, 5) == 0 and G.meta_bytes(3, 0) == 0
     for B, T in [(1, 1), (1, 7), (8, 64), (32, 128), (3, 65), (5, 33)]:
         off = G.meta_layout(B, T)
-        end = off["qoff"] + 4 * B * (T + 1)
+        end = off["ppos"] + 4 * B * T
         assert G.meta_bytes(B, T) == (end + 255) // 256 * 256
-        for k in ("depth", "order", "pos", "parent", "status", "nvalid", "pdep", "ppos", "ancp",
-                  "qoff"):
+        for k in ("depth", "order", "pos", "parent", "status", "nvalid", "pdep", "ppos"):
             assert off[k] % 16 == 0
-        assert off["qoff"] >= off["ancp"] + 8 * B * T * off["W"]
         assert off["depth"] >= 8 * B * T * off["W"]
 
 
