@@ -84,7 +84,7 @@ typedef struct {
   float scale;
 } gdn_dims;
 
-#define GDN_MAX_T 128
+#define GDN_MAX_T 512
 
 /* Size in bytes of the tree-metadata blob for B trees of T slots (host only,
  * no device work).  Layout, W = ceil(T/64); each array starts at the next

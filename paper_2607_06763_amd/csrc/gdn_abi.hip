@@ -40,6 +40,17 @@ static int check_dims(const gdn_dims* d, const char* who) {
   return GDN_OK;
 }
 
+// Verification at any supported T: the LDS-resident kernel up to 128 slots,
+// the feature workspace + gathered pull-back above.
+static int verify_any(const VerifyArgs& a, hipStream_t stream) {
+  if (a.T <= kSmallMaxT) return launch_verify(a, stream);
+  const size_t bytes = large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv);
+  int rc = GDN_OK;
+  void* ws = stream_workspace(bytes, stream, &rc);
+  if (!ws) return rc;
+  return launch_verify_large(a, static_cast<float*>(ws), bytes, stream);
+}
+
 }  // namespace gdn
 
 using namespace gdn;
@@ -90,7 +101,7 @@ int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const
   a.conv_state = conv_state;
   a.S0 = S0;
   a.out = out;
-  return launch_verify(a, stream);
+  return verify_any(a, stream);
 }
 
 int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* q, const void* k,
@@ -203,7 +214,35 @@ int gdn_tree_step(const gdn_dims* dims, const void* prev_meta, const int32_t* pr
   a.conv_state_out = conv_state_out;
   a.S = S;
   a.commit_status = commit_status;
-  return launch_verify(a, stream);
+  if (a.T <= kSmallMaxT) return launch_verify(a, stream);
+  // larger trees: the commit kernels (conv state into conv_state_out), then
+  // the verification against the committed state
+  CommitArgs c;
+  c.B = a.B;
+  c.T = a.T;
+  c.Hk = a.Hk;
+  c.Hv = a.Hv;
+  c.dk = a.dk;
+  c.dv = a.dv;
+  c.in_dtype = a.in_dtype;
+  c.meta = prev_meta;
+  c.accepted = prev_accepted;
+  c.q = prev_q;
+  c.k = prev_k;
+  c.v = prev_v;
+  c.alpha = prev_alpha;
+  c.beta = prev_beta;
+  c.conv_w = conv_w;
+  c.conv_state = conv_state_out;
+  c.conv_state_in = conv_state;
+  c.S = S;
+  c.commit_status = commit_status;
+  rc = launch_commit(c, stream);
+  if (rc != GDN_OK) return rc;
+  VerifyArgs v2 = a;
+  v2.fused = false;
+  v2.conv_state = conv_state_out;
+  return verify_any(v2, stream);
 }
 
 const char* gdn_last_error(void) { return g_err; }

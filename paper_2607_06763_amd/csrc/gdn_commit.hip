@@ -23,7 +23,7 @@ namespace gdn {
 
 // threads per state workgroup: 512, or one per state element for tiny heads
 constexpr int commit_threads(int dk, int dv) { return dk * dv >= 512 ? 512 : dk * dv; }
-constexpr int kCMaxT = 128;    // tree slots supported
+constexpr int kCMaxT = 512;    // tree slots supported
 constexpr int kMH = kMC / 2;   // path nodes per feature half
 
 struct CommitParams {
@@ -32,7 +32,8 @@ struct CommitParams {
   const int32_t* accepted;
   const void *q, *k, *v, *alpha, *beta;
   const float* conv_w;
-  float* conv_state;
+  const float* cs_in;  // conv state before the commit
+  float* cs_out;       // conv state after it (may equal cs_in)
   float* S;
   int32_t* commit_status;
 };
@@ -75,31 +76,28 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
   const TIn* alpha = static_cast<const TIn*>(p.alpha);
   const TIn* beta = static_cast<const TIn*>(p.beta);
 
-  // ---- first load wave: statuses, depths and gates of all slots (raw gates are
-  //      converted only once the path is known)
+  // ---- the accepted slot, then its path root..a read off its ancestor bitmask
   const int a = p.accepted[b];
   const int tree_st = m.status[b];
-  const int tj = tid < T ? tid : T - 1;
-  const int dep_j = m.depth[size_t(b) * T + tj];
-  const TIn al_j = alpha[(size_t(b) * T + tj) * Hv + h];
-  const TIn be_j = beta[(size_t(b) * T + tj) * Hv + h];
   if (tree_st != GDN_TREE_OK || a < 0 || a >= T) {
     if (h == 0 && tid == 0 && p.commit_status)
       p.commit_status[b] = tree_st != GDN_TREE_OK ? tree_st : (a == -1 ? GDN_TREE_OK : GDN_TREE_BAD_ACCEPTED);
     return;
   }
-  // ---- second load wave: the ancestor bitmask of a -> the path root..a
-  const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (tj >> 6)];
-  if (tid < T) s_dep[tid] = dep_j;
+  for (int j = tid; j < T; j += kCT) s_dep[j] = m.depth[size_t(b) * T + j];
   __syncthreads();
   const int d = s_dep[a];
   if (h == 0 && tid == 0 && p.commit_status)
     p.commit_status[b] = d < 0 ? GDN_TREE_BAD_ACCEPTED : GDN_TREE_OK;
   if (d < 0) return;  // accepted slot is padding
-  if (tid < T && (tid == a || ((word >> (tid & 63)) & 1ull))) {
-    s_path[dep_j] = tid;
-    s_al[dep_j] = to_f32(al_j);
-    s_be[dep_j] = to_f32(be_j);
+  for (int j = tid; j < T; j += kCT) {
+    const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (j >> 6)];
+    if (j == a || ((word >> (j & 63)) & 1ull)) {
+      const int dj = s_dep[j];
+      s_path[dj] = j;
+      s_al[dj] = ld(alpha, (size_t(b) * T + j) * Hv + h);
+      s_be[dj] = ld(beta, (size_t(b) * T + j) * Hv + h);
+    }
   }
   __syncthreads();
   const int L = d + 1;  // path length
@@ -115,7 +113,7 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
   const TIn* fsrc = vtask ? static_cast<const TIn*>(p.v) + size_t(b) * T * Hv * DV + size_t(h) * DV + fc
                           : static_cast<const TIn*>(p.k) + size_t(b) * T * Hk * DK + size_t(g) * DK + fc;
   const size_t fstride = vtask ? size_t(Hv) * DV : size_t(Hk) * DK;
-  const float* fcs = p.conv_state + size_t(b) * 3 * C + fch;
+  const float* fcs = p.cs_in + size_t(b) * 3 * C + fch;
   FeatWindow<TIn, kMH> win;
   if (vtask || ktask) win.load(fsrc, fstride, fcs, C, p.conv_w + size_t(fch) * 4, s_path, fhalf * kMH, L);
 
@@ -202,17 +200,25 @@ __global__ __launch_bounds__(256) void commit_conv_kernel(CommitParams p, int DK
   const int T = p.T, Hk = p.Hk, Hv = p.Hv;
   const int C = 2 * Hk * DK + Hv * DV;
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
+  if (c >= C) return;
   const int a = p.accepted[b];
-  if (commit_check(m, b, T, a) != GDN_TREE_OK || a == -1 || c >= C) return;
+  const float* ci = p.cs_in + size_t(b) * 3 * C;
+  float* co = p.cs_out + size_t(b) * 3 * C;
+  float old[3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s) old[s] = ci[size_t(s) * C + c];
+  if (commit_check(m, b, T, a) != GDN_TREE_OK || a == -1) {  // nothing committed
+    if (co != ci) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s) co[size_t(s) * C + c] = old[s];
+    }
+    return;
+  }
   const int L = m.depth[size_t(b) * T + a] + 1;
   int n[3];  // path nodes at distance 0, 1, 2 from the accepted slot
   n[0] = a;
   n[1] = L >= 2 ? m.parent[size_t(b) * T + a] : -1;
   n[2] = L >= 3 ? m.parent[size_t(b) * T + n[1]] : -1;
-  float* cs = p.conv_state + size_t(b) * 3 * C;
-  float old[3];
-#pragma unroll
-  for (int s = 0; s < 3; ++s) old[s] = cs[size_t(s) * C + c];
   const int nq = Hk * DK;
   float nw[3];
 #pragma unroll
@@ -232,7 +238,7 @@ __global__ __launch_bounds__(256) void commit_conv_kernel(CommitParams p, int DK
     }
   }
 #pragma unroll
-  for (int s = 0; s < 3; ++s) cs[size_t(s) * C + c] = nw[s];
+  for (int s = 0; s < 3; ++s) co[size_t(s) * C + c] = nw[s];
 }
 
 template <int DK, int DV, typename TIn>
@@ -286,7 +292,8 @@ int launch_commit(const CommitArgs& a, hipStream_t stream) {
   p.alpha = a.alpha;
   p.beta = a.beta;
   p.conv_w = a.conv_w;
-  p.conv_state = a.conv_state;
+  p.cs_in = a.conv_state_in ? a.conv_state_in : a.conv_state;
+  p.cs_out = a.conv_state;
   p.S = a.S;
   p.commit_status = a.commit_status;
   if (a.in_dtype == GDN_BF16) return commit_dk<BF16>(a, p, stream);

@@ -14,6 +14,7 @@
 namespace gdn {
 
 constexpr int kWave = 64;
+constexpr int kSmallMaxT = 128;  // largest tree of the LDS-resident verify kernel
 constexpr int kPad = -2;   // parent value of an absent slot
 constexpr int kRoot = -1;  // parent value of the root
 
@@ -180,6 +181,46 @@ __device__ __forceinline__ f32x4 mfma3(const bf16x8& ah, const bf16x8& al, const
 }
 
 // ---------------------------------------------------------------------------
+// fp16 operands of the S0 readout: power-of-two row scaling.
+// ---------------------------------------------------------------------------
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Largest magnitude over aligned groups of N consecutive lanes (N <= 32).
+template <int N>
+__device__ __forceinline__ float group_max(float v) {
+  static_assert(N >= 1 && N <= 32 && (N & (N - 1)) == 0, "group size");
+  if constexpr (N >= 2) v = fmaxf(v, dpp_f<kDppQuadXor1>(v));
+  if constexpr (N >= 4) v = fmaxf(v, dpp_f<kDppQuadXor2>(v));
+  if constexpr (N >= 8) v = fmaxf(v, dpp_f<kDppRowHalfMirror>(v));
+  if constexpr (N >= 16) v = fmaxf(v, dpp_f<kDppRowMirror>(v));
+  if constexpr (N >= 32) v = fmaxf(v, __shfl_xor(v, 16));
+  return v;
+}
+
+// Power-of-two row scale for the fp16 S0 plane: for a row whose largest
+// magnitude is m, scale = 2^-floor(log2 m) puts m into [1, 2) and
+// inv = 1 / scale; both are exact.  Zero (or subnormal) rows keep scale 1;
+// the exponent is clamped so that both factors stay normal floats.
+__device__ __forceinline__ void row_scale(float m, float& scale, float& inv) {
+  int ex = int((__float_as_uint(m) >> 23) & 0xffu);
+  if (ex == 0) {
+    scale = inv = 1.0f;
+    return;
+  }
+  ex = ex > 253 ? 253 : ex;
+  scale = __uint_as_float(uint32_t(254 - ex) << 23);
+  inv = __uint_as_float(uint32_t(ex) << 23);
+}
+
+// 4 floats times a scale -> 4 fp16 (round to nearest even), packed in 8 bytes
+__device__ __forceinline__ uint2 to_f16x4(float4 x, float sc) {
+  const _Float16 h0 = (_Float16)(x.x * sc), h1 = (_Float16)(x.y * sc);
+  const _Float16 h2 = (_Float16)(x.z * sc), h3 = (_Float16)(x.w * sc);
+  return make_uint2(uint32_t(__builtin_bit_cast(uint16_t, h0)) | (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16),
+                    uint32_t(__builtin_bit_cast(uint16_t, h2)) | (uint32_t(__builtin_bit_cast(uint16_t, h3)) << 16));
+}
+
+// ---------------------------------------------------------------------------
 // Commit building blocks shared by the commit kernel and the fused step.
 // ---------------------------------------------------------------------------
 constexpr int kMC = 32;  // path nodes featurised per chunk
@@ -240,22 +281,29 @@ __device__ __forceinline__ float replay_rows(float (&sr)[R * CPT], const float (
   }
 #pragma unroll
   for (int i = 0; i < R; ++i) uu[i] = group_sum<LPR>(uu[i]) * inv;  // S_stored . k_hat
-  // c = beta (v_r - alpha S_true.k_hat), scaled into the stored frame and
-  // multiplied by 1 / ||k|| so that it applies to the raw key
+  // c = beta (v_r - alpha S_true.k_hat), multiplied by 1 / ||k|| so that it
+  // applies to the raw key
   const float ag = al * gamma;
-  const float ri = __builtin_amdgcn_rcpf(ag) * inv;
+  if (ag >= 0x1p-60f) {
+    // stored frame: S_true' = ag (stored + c / ag k)
+    const float ri = __builtin_amdgcn_rcpf(ag) * inv;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const float c = be * (vr[i] - ag * uu[i]) * ri;
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) sr[i * CPT + e] += c * kk[e];
+    }
+    return ag;
+  }
+  // tiny decay (uniform branch): the step is taken in the true frame,
+  // S_true' = ag stored + c k, with no division by ag (which may be 0)
 #pragma unroll
   for (int i = 0; i < R; ++i) {
-    const float c = be * (vr[i] - ag * uu[i]) * ri;
+    const float c = be * (vr[i] - ag * uu[i]) * inv;
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) sr[i * CPT + e] += c * kk[e];
+    for (int e = 0; e < CPT; ++e) sr[i * CPT + e] = fmaf(ag, sr[i * CPT + e], c * kk[e]);
   }
-  if (ag < 0x1p-60f) {  // keep the stored frame in range (uniform branch)
-#pragma unroll
-    for (int e = 0; e < R * CPT; ++e) sr[e] *= ag;
-    return 1.0f;
-  }
-  return ag;
+  return 1.0f;
 }
 
 // CPT floats of an LDS row (16-byte pieces when CPT % 4 == 0)
@@ -299,6 +347,13 @@ struct VerifyArgs {
   int32_t* commit_status = nullptr;
 };
 int launch_verify(const VerifyArgs& a, hipStream_t stream);
+// trees of 129..512 slots: features into the workspace, then the pull-back
+// (the workspace holds large_workspace_bytes(...) bytes)
+size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv);
+int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStream_t stream);
+// A device buffer of at least bytes for work on stream, cached per (device,
+// stream) and grown on demand (never while the stream is being captured).
+void* stream_workspace(size_t bytes, hipStream_t stream, int* rc);
 // the paper's chunked form (Eq. 9-13) of the same verification
 int launch_verify_chunked(const VerifyArgs& a, hipStream_t stream);
 
@@ -308,7 +363,8 @@ struct CommitArgs {
   const int32_t* accepted;
   const void *q, *k, *v, *alpha, *beta;
   const float* conv_w;
-  float* conv_state;
+  float* conv_state;                      // in/out, or out when conv_state_in is set
+  const float* conv_state_in = nullptr;   // conv state before the commit (not in place)
   float* S;
   int32_t* commit_status;
 };

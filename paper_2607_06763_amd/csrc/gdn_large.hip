@@ -1,0 +1,412 @@
+// gdn_large.hip -- read-only verification of trees of 129..512 slots.
+//
+// The verification of one node is the query pull-back of the T <= 128
+// kernel (an exact rearrangement of Eq. 7-8): walking the path of i from
+// the node to the root with
+//     x <- q~_i, r <- 1, acc <- 0;   for t = i, parent(i), ..., root:
+//         s = k~_t.x;  acc += r beta_t s v~_t;  x <- x - beta_t s k~_t;  r <- r alpha_t
+// gives o_i = scale (S0 (r x) + acc) in the stored orientation.  With up to
+// 512 slots the post-conv features of a tree no longer fit in LDS, so the
+// work is split in two launches:
+//   feat_kernel   one workgroup per (position, sequence): the width-4 conv
+//                 along the node's path (conv-state slots above the root),
+//                 SiLU, and the per-head L2 norm of q and k, for every
+//                 channel; written to a workspace F[B][T][C] (fp32, canonical
+//                 position order, channels as in conv_w)
+//   pull_kernel   one workgroup per (value head, sequence), 512 threads:
+//                 the head's S0 as one fp16 plane in LDS (each row scaled by
+//                 the power of two that puts its largest magnitude in [1, 2),
+//                 exact, undone on the output), then tiles of 32 positions:
+//                 16 lanes per node walk the paths with the features of the
+//                 path nodes gathered from F (one step of loads ahead),
+//                 r x -> an fp16 tile, O^T = S0 (r X)^T on
+//                 v_mfma_f32_16x16x32_f16 (fp32 accumulation), plus acc.
+#include <map>
+#include <mutex>
+
+#include "gdn_internal.h"
+
+namespace gdn {
+
+constexpr int kLT = 512;      // threads of a pull-back workgroup (8 waves)
+constexpr int kLTile = 32;    // positions per readout tile (4 per wave)
+constexpr int kLMaxT = 512;   // tree slots supported
+constexpr int kFT = 256;      // threads of a feature workgroup
+
+struct LargeParams {
+  int B, T, Hk, Hv;
+  float scale;
+  const void* meta;
+  const void *q, *k, *v, *alpha, *beta;
+  const float *conv_w, *conv_state, *S0;
+  float* out;
+  float* F;  // workspace [B][T][C]
+};
+
+size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
+  return size_t(B) * size_t(T) * size_t(2 * Hk * dk + Hv * dv) * sizeof(float);
+}
+
+// ---------------------------------------------------------------------------
+// Features of one position: conv taps along the path, SiLU, L2 norm (q, k)
+// ---------------------------------------------------------------------------
+template <typename TIn, int DK>
+__global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
+  const int pos = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int T = p.T, Hk = p.Hk, Hv = p.Hv;
+  const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
+  if (m.status[b] != GDN_TREE_OK || pos >= m.nvalid[b]) return;  // uniform
+  const size_t bt = size_t(b) * T;
+  const int nq = Hk * DK;
+  const int C = 2 * nq + Hv * DV;
+  // the 4 taps (3 = the node itself): a path node's raw row, or the
+  // conv-state slot d + w for taps above the root
+  const int d = m.pdep[bt + pos];
+  const int t2 = m.ppos[bt + pos];
+  const int t1 = t2 >= 0 ? m.ppos[bt + t2] : -1;
+  const int t0 = t1 >= 0 ? m.ppos[bt + t1] : -1;
+  const int tp[4] = {t0, t1, t2, pos};
+  int node[4];
+#pragma unroll
+  for (int w = 0; w < 4; ++w) node[w] = d - 3 + w >= 0 ? m.order[bt + tp[w]] : -1 - (d + w);
+  const TIn* q = static_cast<const TIn*>(p.q);
+  const TIn* k = static_cast<const TIn*>(p.k);
+  const TIn* v = static_cast<const TIn*>(p.v);
+  const float* cs = p.conv_state + size_t(b) * 3 * C;
+  float* dst = p.F + (bt + pos) * size_t(C);
+  const int n4 = C / 4;
+  // uniform trip count: every lane takes part in the group sums
+  for (int it = 0; it < (n4 + kFT - 1) / kFT; ++it) {
+    const int c4 = it * kFT + tid;
+    const bool ok = c4 < n4;
+    const int c = ok ? 4 * c4 : 0;
+    float4 x[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int nd = node[w];
+      if (nd < 0) {
+        x[w] = ld4(cs + size_t(-1 - nd) * C + c);
+      } else if (c < nq) {
+        x[w] = ld4(q + (bt + nd) * nq + c);
+      } else if (c < 2 * nq) {
+        x[w] = ld4(k + (bt + nd) * nq + (c - nq));
+      } else {
+        x[w] = ld4(v + (bt + nd) * size_t(Hv) * DV + (c - 2 * nq));
+      }
+    }
+    const float4* wr = reinterpret_cast<const float4*>(p.conv_w + size_t(c) * 4);
+    const float4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
+    float y[4];
+    y[0] = silu(fmaf(w0.w, x[3].x, fmaf(w0.z, x[2].x, fmaf(w0.y, x[1].x, w0.x * x[0].x))));
+    y[1] = silu(fmaf(w1.w, x[3].y, fmaf(w1.z, x[2].y, fmaf(w1.y, x[1].y, w1.x * x[0].y))));
+    y[2] = silu(fmaf(w2.w, x[3].z, fmaf(w2.z, x[2].z, fmaf(w2.y, x[1].z, w2.x * x[0].z))));
+    y[3] = silu(fmaf(w3.w, x[3].w, fmaf(w3.z, x[2].w, fmaf(w3.y, x[1].w, w3.x * x[0].w))));
+    // the DK / 4 lanes of a q or k head are consecutive lanes of one wave
+    float ss = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
+    ss = group_sum<DK / 4>(ss);
+    const float f = c < 2 * nq ? rsqrt_hw(ss + 1e-6f) : 1.0f;
+    if (ok) *reinterpret_cast<float4*>(dst + c) = make_float4(y[0] * f, y[1] * f, y[2] * f, y[3] * f);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pull-back along gathered features + fp16 MFMA readout
+// ---------------------------------------------------------------------------
+template <int DK, int DV>
+struct PullSmem {
+  static constexpr int KP = (DK < 32 ? 32 : DK) + 8;  // fp16 row (zero beyond DK)
+  static constexpr int PP = DV + 4;                    // fp32 row of the product tile
+  static constexpr size_t plane = size_t(DV) * KP * 2;
+  static constexpr size_t xt = size_t(kLTile) * KP * 2;
+  static constexpr size_t pt = size_t(kLTile) * PP * 4;
+  static constexpr size_t inv = size_t(DV) * 4;
+  static constexpr size_t meta = size_t(kLMaxT) * (2 + 2 + 4 + 4);
+  static constexpr size_t total = plane + xt + pt + inv + meta;
+};
+
+template <int N>
+__device__ __forceinline__ void ld_f(const float* src, float (&x)[N]) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int e = 0; e < N; e += 4) {
+      const float4 u = *reinterpret_cast<const float4*>(src + e);
+      x[e] = u.x;
+      x[e + 1] = u.y;
+      x[e + 2] = u.z;
+      x[e + 3] = u.w;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < N; ++e) x[e] = src[e];
+  }
+}
+
+template <int DK, int DV, typename TIn>
+__global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
+  using SM = PullSmem<DK, DV>;
+  constexpr int KP = SM::KP, PP = SM::PP;
+  constexpr int CK = DK / 16, CV = DV / 16;  // channels per lane (16 lanes per node)
+  constexpr int KS = (DK < 32 ? 32 : DK) / 32;
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16* s_plane = reinterpret_cast<_Float16*>(smem);
+  _Float16* s_x = reinterpret_cast<_Float16*>(smem + SM::plane);
+  float* s_p = reinterpret_cast<float*>(smem + SM::plane + SM::xt);
+  float* s_inv = reinterpret_cast<float*>(smem + SM::plane + SM::xt + SM::pt);
+  int16_t* s_ord = reinterpret_cast<int16_t*>(smem + SM::plane + SM::xt + SM::pt + SM::inv);
+  int16_t* s_ppos = s_ord + kLMaxT;
+  float* s_al = reinterpret_cast<float*>(s_ppos + kLMaxT);
+  float* s_be = s_al + kLMaxT;
+
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int T = p.T, Hk = p.Hk, Hv = p.Hv;
+  const int g = h * Hk / Hv;
+  const int nq = Hk * DK;
+  const size_t C = size_t(2 * nq + Hv * DV);
+  const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
+  const size_t bt = size_t(b) * T;
+  const int nval = m.status[b] == GDN_TREE_OK ? m.nvalid[b] : 0;
+  const TIn* alpha = static_cast<const TIn*>(p.alpha);
+  const TIn* beta = static_cast<const TIn*>(p.beta);
+
+  // ---- tree metadata and this head's gates by position
+  for (int j = tid; j < T; j += kLT) {
+    const int nd = m.order[bt + j];
+    s_ord[j] = int16_t(nd);
+    s_ppos[j] = int16_t(j < nval ? m.ppos[bt + j] : -1);
+    s_al[j] = j < nval ? ld(alpha, (bt + nd) * Hv + h) : 0.0f;
+    s_be[j] = j < nval ? ld(beta, (bt + nd) * Hv + h) : 0.0f;
+  }
+  // ---- S0 -> fp16 plane (16 lanes per row), zero columns past DK
+  if (nval > 0) {
+    const float* S0 = p.S0 + (size_t(b) * Hv + h) * size_t(DV) * DK;
+    const int ln = tid & 15;
+    for (int r0 = 0; r0 < DV; r0 += kLT / 16) {
+      const int r = r0 + (tid >> 4);
+      if (r < DV) {  // uniform per 16-lane group
+        float xs[CK];
+        ld_f<CK>(S0 + size_t(r) * DK + ln * CK, xs);
+        float mx = 0.0f;
+#pragma unroll
+        for (int e = 0; e < CK; ++e) mx = fmaxf(mx, fabsf(xs[e]));
+        mx = group_max<16>(mx);
+        float sc, inv;
+        row_scale(mx, sc, inv);
+#pragma unroll
+        for (int e = 0; e < CK; ++e) s_plane[r * KP + ln * CK + e] = (_Float16)(xs[e] * sc);
+        if (ln == 0) s_inv[r] = inv;
+      }
+    }
+    if constexpr (DK < 32) {
+      for (int i = tid; i < DV * (32 - DK); i += kLT)
+        s_plane[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
+      for (int i = tid; i < kLTile * (32 - DK); i += kLT)
+        s_x[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
+    }
+  }
+  __syncthreads();
+
+  const float scale = p.scale;
+  const int jn = wave * 4 + (lane >> 4);  // node slot of this lane in a tile
+  const int ln = lane & 15;
+  const float* Fb = p.F + bt * C;
+  for (int n0 = 0; n0 < T; n0 += kLTile) {
+    const int pos = n0 + jn;
+    const bool real = pos < nval;
+    float x[CK], acc[CV];
+    float r = 1.0f;
+#pragma unroll
+    for (int e = 0; e < CV; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int e = 0; e < CK; ++e) x[e] = 0.0f;
+    if (real) {
+      ld_f<CK>(Fb + size_t(pos) * C + g * DK + ln * CK, x);
+      // walk to the root; the path node's features load one step ahead
+      int t = pos;
+      float kc[CK], vc[CV];
+      ld_f<CK>(Fb + size_t(t) * C + nq + g * DK + ln * CK, kc);
+      ld_f<CV>(Fb + size_t(t) * C + 2 * nq + h * DV + ln * CV, vc);
+      while (t >= 0) {  // uniform per 16-lane node group
+        const int tn = s_ppos[t];
+        float kn[CK], vn[CV];
+        if (tn >= 0) {
+          ld_f<CK>(Fb + size_t(tn) * C + nq + g * DK + ln * CK, kn);
+          ld_f<CV>(Fb + size_t(tn) * C + 2 * nq + h * DV + ln * CV, vn);
+        } else {
+#pragma unroll
+          for (int e = 0; e < CK; ++e) kn[e] = 0.0f;
+#pragma unroll
+          for (int e = 0; e < CV; ++e) vn[e] = 0.0f;
+        }
+        float s = 0.0f;
+#pragma unroll
+        for (int e = 0; e < CK; ++e) s = fmaf(kc[e], x[e], s);
+        s = group_sum<16>(s);
+        const float c = s_be[t] * s;
+        const float rc = r * c;
+#pragma unroll
+        for (int e = 0; e < CV; ++e) acc[e] = fmaf(rc, vc[e], acc[e]);
+#pragma unroll
+        for (int e = 0; e < CK; ++e) x[e] = fmaf(-c, kc[e], x[e]);
+        r *= s_al[t];
+        t = tn;
+#pragma unroll
+        for (int e = 0; e < CK; ++e) kc[e] = kn[e];
+#pragma unroll
+        for (int e = 0; e < CV; ++e) vc[e] = vn[e];
+      }
+    }
+    // r x -> fp16 tile row jn (zero for padding positions)
+#pragma unroll
+    for (int e = 0; e < CK; ++e) s_x[jn * KP + ln * CK + e] = (_Float16)(r * x[e]);
+    __syncthreads();
+    // O^T tiles (16 value rows x 16 positions), K = key channels
+    {
+      const int l16 = lane & 15, lg = lane >> 4;
+      for (int task = wave; task < (DV / 16) * (kLTile / 16); task += kLT / 64) {
+        const int rt = task / (kLTile / 16), ct = task % (kLTile / 16);
+        f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const f16x8 a = *reinterpret_cast<const f16x8*>(s_plane + (16 * rt + l16) * KP + 32 * ks + 8 * lg);
+          const f16x8 bx = *reinterpret_cast<const f16x8*>(s_x + (16 * ct + l16) * KP + 32 * ks + 8 * lg);
+          acc4 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bx, acc4, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * rt + 4 * lg + i;
+          s_p[(16 * ct + l16) * PP + row] = acc4[i] * s_inv[row];
+        }
+      }
+    }
+    __syncthreads();
+    if (pos < T) {
+      float o[CV];
+#pragma unroll
+      for (int e = 0; e < CV; ++e) o[e] = real ? scale * (s_p[jn * PP + ln * CV + e] + acc[e]) : 0.0f;
+      float* dst = p.out + (bt + s_ord[pos]) * size_t(Hv) * DV + size_t(h) * DV + ln * CV;
+      if constexpr (CV % 4 == 0) {
+#pragma unroll
+        for (int e = 0; e < CV; e += 4)
+          *reinterpret_cast<float4*>(dst + e) = make_float4(o[e], o[e + 1], o[e + 2], o[e + 3]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < CV; ++e) dst[e] = o[e];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launch
+// ---------------------------------------------------------------------------
+template <int DK, int DV, typename TIn>
+static int launch_large_t(const LargeParams& p, hipStream_t stream) {
+  const int C = 2 * p.Hk * DK + p.Hv * DV;
+  (void)C;
+  hipLaunchKernelGGL((feat_kernel<TIn, DK>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, DV);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
+  using SM = PullSmem<DK, DV>;
+  static bool attr = false;  // the maximum dynamic LDS is set once per process
+  if (!attr) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&pull_kernel<DK, DV, TIn>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, int(SM::total));
+    if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) LDS attribute: %s", hipGetErrorString(e));
+    attr = true;
+  }
+  hipLaunchKernelGGL((pull_kernel<DK, DV, TIn>), dim3(p.Hv, p.B), dim3(kLT), SM::total, stream, p);
+  e = hipGetLastError();
+  if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) launch: %s", hipGetErrorString(e));
+  return GDN_OK;
+}
+
+template <int DK, typename TIn>
+static int large_dv(const VerifyArgs& a, const LargeParams& p, hipStream_t s) {
+  switch (a.dv) {
+    case 16: return launch_large_t<DK, 16, TIn>(p, s);
+    case 32: return launch_large_t<DK, 32, TIn>(p, s);
+    case 64: return launch_large_t<DK, 64, TIn>(p, s);
+    case 128: return launch_large_t<DK, 128, TIn>(p, s);
+  }
+  return set_error(GDN_EUNSUPPORTED, "verify: dv=%d unsupported", a.dv);
+}
+
+template <typename TIn>
+static int large_dk(const VerifyArgs& a, const LargeParams& p, hipStream_t s) {
+  switch (a.dk) {
+    case 16: return large_dv<16, TIn>(a, p, s);
+    case 32: return large_dv<32, TIn>(a, p, s);
+    case 64: return large_dv<64, TIn>(a, p, s);
+    case 128: return large_dv<128, TIn>(a, p, s);
+  }
+  return set_error(GDN_EUNSUPPORTED, "verify: dk=%d unsupported", a.dk);
+}
+
+int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStream_t stream) {
+  if (a.T > kLMaxT) return set_error(GDN_EUNSUPPORTED, "verify: T=%d exceeds %d", a.T, kLMaxT);
+  if (ws_bytes < large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv))
+    return set_error(GDN_EINVAL, "verify: workspace of %zu bytes is too small", ws_bytes);
+  LargeParams p;
+  p.B = a.B;
+  p.T = a.T;
+  p.Hk = a.Hk;
+  p.Hv = a.Hv;
+  p.scale = a.scale;
+  p.meta = a.meta;
+  p.q = a.q;
+  p.k = a.k;
+  p.v = a.v;
+  p.alpha = a.alpha;
+  p.beta = a.beta;
+  p.conv_w = a.conv_w;
+  p.conv_state = a.conv_state;
+  p.S0 = a.S0;
+  p.out = a.out;
+  p.F = ws;
+  if (a.in_dtype == GDN_BF16) return large_dk<BF16>(a, p, stream);
+  return large_dk<float>(a, p, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Workspace of the T > 128 path: one device buffer per (device, stream),
+// grown on demand and kept until the process ends.
+// ---------------------------------------------------------------------------
+void* stream_workspace(size_t bytes, hipStream_t stream, int* rc) {
+  static std::mutex mu;
+  static std::map<std::pair<int, hipStream_t>, std::pair<void*, size_t>> bufs;
+  *rc = GDN_OK;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    *rc = set_error(GDN_EHIP, "workspace: hipGetDevice failed");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  auto& e = bufs[{dev, stream}];
+  if (e.second >= bytes) return e.first;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    *rc = set_error(GDN_EUNSUPPORTED,
+                    "workspace: %zu bytes needed while the stream is captured; run the same sizes once "
+                    "uncaptured first",
+                    bytes);
+    return nullptr;
+  }
+  if (e.first) {  // only this stream used it
+    if (hipStreamSynchronize(stream) != hipSuccess || hipFree(e.first) != hipSuccess) {
+      *rc = set_error(GDN_EHIP, "workspace: release of %zu bytes failed", e.second);
+      return nullptr;
+    }
+    e.first = nullptr;
+    e.second = 0;
+  }
+  if (hipMalloc(&e.first, bytes) != hipSuccess) {
+    e.first = nullptr;
+    *rc = set_error(GDN_EHIP, "workspace: hipMalloc of %zu bytes failed", bytes);
+    return nullptr;
+  }
+  e.second = bytes;
+  return e.first;
+}
+
+}  // namespace gdn

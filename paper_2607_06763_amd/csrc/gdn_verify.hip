@@ -199,43 +199,6 @@ __device__ __forceinline__ float lane_gather(float v, int src) {
   return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(v)));
 }
 
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-
-// Largest magnitude over aligned groups of N consecutive lanes (N <= 32).
-template <int N>
-__device__ __forceinline__ float group_max(float v) {
-  static_assert(N >= 1 && N <= 32 && (N & (N - 1)) == 0, "group size");
-  if constexpr (N >= 2) v = fmaxf(v, dpp_f<kDppQuadXor1>(v));
-  if constexpr (N >= 4) v = fmaxf(v, dpp_f<kDppQuadXor2>(v));
-  if constexpr (N >= 8) v = fmaxf(v, dpp_f<kDppRowHalfMirror>(v));
-  if constexpr (N >= 16) v = fmaxf(v, dpp_f<kDppRowMirror>(v));
-  if constexpr (N >= 32) v = fmaxf(v, __shfl_xor(v, 16));
-  return v;
-}
-
-// Power-of-two row scale for the fp16 S0 plane: for a row whose largest
-// magnitude is m, scale = 2^-floor(log2 m) puts m into [1, 2) and
-// inv = 1 / scale; both are exact.  Zero (or subnormal) rows keep scale 1;
-// the exponent is clamped so that both factors stay normal floats.
-__device__ __forceinline__ void row_scale(float m, float& scale, float& inv) {
-  int ex = int((__float_as_uint(m) >> 23) & 0xffu);
-  if (ex == 0) {
-    scale = inv = 1.0f;
-    return;
-  }
-  ex = ex > 253 ? 253 : ex;
-  scale = __uint_as_float(uint32_t(254 - ex) << 23);
-  inv = __uint_as_float(uint32_t(ex) << 23);
-}
-
-// 4 floats times a scale -> 4 fp16 (round to nearest even), packed in 8 bytes
-__device__ __forceinline__ uint2 to_f16x4(float4 x, float sc) {
-  const _Float16 h0 = (_Float16)(x.x * sc), h1 = (_Float16)(x.y * sc);
-  const _Float16 h2 = (_Float16)(x.z * sc), h3 = (_Float16)(x.w * sc);
-  return make_uint2(uint32_t(__builtin_bit_cast(uint16_t, h0)) | (uint32_t(__builtin_bit_cast(uint16_t, h1)) << 16),
-                    uint32_t(__builtin_bit_cast(uint16_t, h2)) | (uint32_t(__builtin_bit_cast(uint16_t, h3)) << 16));
-}
-
 // LDS regions (bytes) for a tree of T slots, key dim DK and value slice DVS
 struct VerifySmem {
   size_t rk, rv, meta, p0, total;

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libgdntree.so")
 GDN_OK, GDN_EINVAL, GDN_EUNSUPPORTED, GDN_EHIP = 0, -1, -2, -3
 GDN_F32, GDN_BF16 = 0, 1
 TREE_OK, TREE_NO_ROOT, TREE_MULTI_ROOT, TREE_BAD_PARENT, TREE_CYCLE, TREE_BAD_ACCEPTED = range(6)
-MAX_T = 128
+MAX_T = 512
 
 EXPORTS = ("gdn_tree_meta_bytes", "gdn_tree_prepare", "gdn_tree_verify",
            "gdn_tree_verify_chunked", "gdn_tree_commit", "gdn_tree_step", "gdn_last_error",

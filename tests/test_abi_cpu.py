@@ -70,7 +70,7 @@ def test_host_validation_errors(L):
         (G.make_dims(-1, 7, 2, 2, 16, 16), G.GDN_EINVAL),        # B < 0
         (G.make_dims(1, 7, 2, 2, 24, 16), G.GDN_EUNSUPPORTED),   # dk
         (G.make_dims(1, 7, 2, 2, 16, 256), G.GDN_EUNSUPPORTED),  # dv
-        (G.make_dims(1, 129, 2, 2, 16, 16), G.GDN_EUNSUPPORTED),  # T > 128
+        (G.make_dims(1, 513, 2, 2, 16, 16), G.GDN_EUNSUPPORTED),  # T > 512
         (G.Dims(1, 7, 2, 2, 16, 16, 5, 0.0), G.GDN_EINVAL),      # dtype
         (G.Dims(1, 7, 2, 2, 16, 16, 0, -1.0), G.GDN_EINVAL),     # scale
     ]
@@ -113,7 +113,7 @@ def test_step_host_validation(L):
     assert "overlap" in G.last_error()
     # shape errors come first; empty problems succeed without touching pointers
     assert _call_step(L, G.make_dims(1, 7, 2, 3, 16, 16), good) == G.GDN_EINVAL
-    assert _call_step(L, G.make_dims(1, 200, 2, 2, 16, 16), good) == G.GDN_EUNSUPPORTED
+    assert _call_step(L, G.make_dims(1, 513, 2, 2, 16, 16), good) == G.GDN_EUNSUPPORTED
     assert _call_step(L, G.make_dims(0, 7, 2, 2, 16, 16), [0] * 19) == G.GDN_OK
 
 
