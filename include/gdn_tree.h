@@ -133,6 +133,23 @@ int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const
                     const void* v, const void* alpha, const void* beta, const float* conv_w,
                     const float* conv_state, const float* S0, float* out, hipStream_t stream);
 
+/* gdn_tree_verify for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops that forbid hipMalloc).  Same
+ * arguments, layouts, outputs and errors as gdn_tree_verify, whose kernels
+ * it runs; it calls no allocating routine.  Trees of more than 128 slots
+ * need a feature workspace of B * T * C * 4 bytes (C = 2 Hk dk + Hv dv):
+ * here it is a static device array of GDN_NOALLOC_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends, and
+ * larger problems return GDN_EUNSUPPORTED before any device work.  All
+ * calls on one device share that array: calls that overlap in time on one
+ * device (different streams, or host threads) race and must be serialized
+ * by the caller. */
+#define GDN_NOALLOC_SCRATCH_BYTES (64u << 20)
+int gdn_tree_verify_noalloc(const gdn_dims* dims, const void* meta, const void* q, const void* k,
+                            const void* v, const void* alpha, const void* beta,
+                            const float* conv_w, const float* conv_state, const float* S0,
+                            float* out, hipStream_t stream);
+
 /* The same verification in the paper's chunked form (Sec. 3.4.1, Eq. 9-13):
  * per (sequence, value head) the interaction matrices X (strict ancestors,
  * decayed key-key products scaled by beta) and Y (ancestors and self, decayed

@@ -104,6 +104,42 @@ int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const
   return verify_any(a, stream);
 }
 
+int gdn_tree_verify_noalloc(const gdn_dims* dims, const void* meta, const void* q, const void* k,
+                            const void* v, const void* alpha, const void* beta, const float* conv_w,
+                            const float* conv_state, const float* S0, float* out, hipStream_t stream) {
+  int rc = check_dims(dims, "verify_noalloc");
+  if (rc != GDN_OK) return rc;
+  if (dims->B == 0 || dims->T == 0) return GDN_OK;
+  const size_t need = dims->T > kSmallMaxT ? large_workspace_bytes(dims->B, dims->T, dims->Hk, dims->Hv,
+                                                                   dims->dk, dims->dv)
+                                           : 0;
+  if (need > size_t(GDN_NOALLOC_SCRATCH_BYTES))
+    return set_error(GDN_EUNSUPPORTED, "verify_noalloc: B=%d T=%d needs %zu workspace bytes, above %zu",
+                     dims->B, dims->T, need, size_t(GDN_NOALLOC_SCRATCH_BYTES));
+  if (!meta || !q || !k || !v || !alpha || !beta || !conv_w || !conv_state || !S0 || !out)
+    return set_error(GDN_EINVAL, "verify_noalloc: NULL tensor pointer");
+  VerifyArgs a;
+  a.B = dims->B;
+  a.T = dims->T;
+  a.Hk = dims->Hk;
+  a.Hv = dims->Hv;
+  a.dk = dims->dk;
+  a.dv = dims->dv;
+  a.in_dtype = dims->in_dtype;
+  a.scale = dims->scale > 0.0f ? dims->scale : 1.0f / sqrtf(float(dims->dk));
+  a.meta = meta;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.conv_w = conv_w;
+  a.conv_state = conv_state;
+  a.S0 = S0;
+  a.out = out;
+  return launch_verify_noalloc(a, stream);
+}
+
 int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* q, const void* k,
                             const void* v, const void* alpha, const void* beta, const float* conv_w,
                             const float* conv_state, const float* S0, float* out, hipStream_t stream) {

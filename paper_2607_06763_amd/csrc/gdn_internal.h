@@ -354,6 +354,9 @@ int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStre
 // A device buffer of at least bytes for work on stream, cached per (device,
 // stream) and grown on demand (never while the stream is being captured).
 void* stream_workspace(size_t bytes, hipStream_t stream, int* rc);
+// gdn_tree_verify without any allocation: the workspace of T > 128 is the
+// library's static device array
+int launch_verify_noalloc(const VerifyArgs& a, hipStream_t stream);
 // the paper's chunked form (Eq. 9-13) of the same verification
 int launch_verify_chunked(const VerifyArgs& a, hipStream_t stream);
 

@@ -369,6 +369,53 @@ int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStre
 }
 
 // ---------------------------------------------------------------------------
+// Allocation-free variant: the workspace is a file-scope device array of
+// GDN_NOALLOC_SCRATCH_BYTES (every device the library runs on holds one
+// copy until the process ends).  In host code `scratch` only names the
+// symbol; its device address is looked up once per device with
+// hipGetSymbolAddress and only that address is passed to kernels.  Calls
+// that overlap on one device share the array and race.  The features are
+// written before they are read, so nothing needs clearing.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[GDN_NOALLOC_SCRATCH_BYTES];
+
+static void* scratch_address(int* rc) {
+  static std::mutex mu;
+  static std::map<int, void*> addr;  // device -> address of its copy
+  *rc = GDN_OK;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    *rc = set_error(GDN_EHIP, "verify_noalloc: hipGetDevice failed");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = addr.find(dev);
+  if (it != addr.end()) return it->second;
+  void* ptr = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || ptr == nullptr) {
+    *rc = set_error(GDN_EHIP, "verify_noalloc: hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    return nullptr;
+  }
+  addr[dev] = ptr;
+  return ptr;
+}
+
+int launch_verify_noalloc(const VerifyArgs& a, hipStream_t stream) {
+  if (a.T <= kSmallMaxT) return launch_verify(a, stream);  // uses no workspace
+  const size_t bytes = large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv);
+  if (bytes > size_t(GDN_NOALLOC_SCRATCH_BYTES))
+    return set_error(GDN_EUNSUPPORTED,
+                     "verify_noalloc: B=%d T=%d needs %zu workspace bytes, above the static %zu (call "
+                     "gdn_tree_verify, or split the batch)",
+                     a.B, a.T, bytes, size_t(GDN_NOALLOC_SCRATCH_BYTES));
+  int rc = GDN_OK;
+  void* ws = scratch_address(&rc);
+  if (!ws) return rc;
+  return launch_verify_large(a, static_cast<float*>(ws), size_t(GDN_NOALLOC_SCRATCH_BYTES), stream);
+}
+
+// ---------------------------------------------------------------------------
 // Workspace of the T > 128 path: one device buffer per (device, stream),
 // grown on demand and kept until the process ends.
 // ---------------------------------------------------------------------------

@@ -20,8 +20,9 @@ TREE_OK, TREE_NO_ROOT, TREE_MULTI_ROOT, TREE_BAD_PARENT, TREE_CYCLE, TREE_BAD_AC
 MAX_T = 512
 
 EXPORTS = ("gdn_tree_meta_bytes", "gdn_tree_prepare", "gdn_tree_verify",
-           "gdn_tree_verify_chunked", "gdn_tree_commit", "gdn_tree_step", "gdn_last_error",
-           "gdn_version")
+           "gdn_tree_verify_noalloc", "gdn_tree_verify_chunked", "gdn_tree_commit",
+           "gdn_tree_step", "gdn_last_error", "gdn_version")
+NOALLOC_SCRATCH_BYTES = 64 << 20  # GDN_NOALLOC_SCRATCH_BYTES of gdn_tree.h
 
 
 class GdnError(RuntimeError):
@@ -66,6 +67,8 @@ def lib() -> ctypes.CDLL:
         L.gdn_tree_prepare.argtypes = [ctypes.POINTER(Dims), vp, vp, vp, vp]
         L.gdn_tree_verify.restype = ctypes.c_int
         L.gdn_tree_verify.argtypes = [ctypes.POINTER(Dims)] + [vp] * 11
+        L.gdn_tree_verify_noalloc.restype = ctypes.c_int
+        L.gdn_tree_verify_noalloc.argtypes = [ctypes.POINTER(Dims)] + [vp] * 11
         L.gdn_tree_verify_chunked.restype = ctypes.c_int
         L.gdn_tree_verify_chunked.argtypes = [ctypes.POINTER(Dims)] + [vp] * 11
         L.gdn_tree_commit.restype = ctypes.c_int
@@ -139,12 +142,16 @@ def prepare(d: Dims, parent, meta, tree_status=None, stream=None) -> None:
 
 
 def verify(d: Dims, meta, q, k, v, alpha, beta, conv_w, conv_state, S0, out, stream=None,
-           chunked: bool = False) -> None:
+           chunked: bool = False, noalloc: bool = False) -> None:
     """gdn_tree_verify (or gdn_tree_verify_chunked, the paper's chunked
-    form): per-node outputs out fp32 [B][T][Hv][dv]."""
+    form, or gdn_tree_verify_noalloc, which allocates nothing): per-node
+    outputs out fp32 [B][T][Hv][dv]."""
     import torch
     f32, it = torch.float32, _in_dtype(d)
-    fn = lib().gdn_tree_verify_chunked if chunked else lib().gdn_tree_verify
+    if chunked and noalloc:
+        raise ValueError("chunked and noalloc are separate entry points")
+    fn = (lib().gdn_tree_verify_chunked if chunked else
+          lib().gdn_tree_verify_noalloc if noalloc else lib().gdn_tree_verify)
     _check(fn(
         ctypes.byref(d), _ptr(meta, (meta_bytes(d.B, d.T),), torch.uint8, "meta"),
         _ptr(q, (d.B, d.T, d.Hk, d.dk), it, "q"), _ptr(k, (d.B, d.T, d.Hk, d.dk), it, "k"),
@@ -232,10 +239,12 @@ class DeviceTree:
     def prepare(self, stream=None):
         prepare(self.dims, self.parent, self.meta, self.tree_status, stream)
 
-    def verify(self, S0=None, conv_state=None, out=None, stream=None, chunked=False):
+    def verify(self, S0=None, conv_state=None, out=None, stream=None, chunked=False,
+               noalloc=False):
         verify(self.dims, self.meta, self.q, self.k, self.v, self.alpha, self.beta, self.conv_w,
                self.conv_state if conv_state is None else conv_state,
-               self.S0 if S0 is None else S0, self.out if out is None else out, stream, chunked)
+               self.S0 if S0 is None else S0, self.out if out is None else out, stream, chunked,
+               noalloc)
 
     def commit(self, S, conv_state, accepted=None, stream=None):
         commit(self.dims, self.meta, self.accepted if accepted is None else accepted, self.q,

@@ -1,0 +1,67 @@
+"""The allocation-free verify entry point, gdn_tree_verify_noalloc, through
+the C ABI: its outputs must equal those of gdn_tree_verify on the same
+inputs (they run the same kernels; the workspace of trees above 128 slots
+is the library's static device array instead of an allocated buffer), on
+consecutive calls whose second input is smaller, and meet the oracle bar
+(2e-3 max|o_ref|).  Sizes beyond the static array are refused before any
+device work."""
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2607_06763_amd import workloads as W
+from tests.guard import check_guards, guarded
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_06763_amd import gdn_tree as G
+    G.lib()
+    return G
+
+
+CALLS = [
+    # (seed, B, T, Hk, Hv, dk, dv, dtype, n_valid): decreasing input sizes
+    (8100, 2, 512, 2, 4, 128, 128, "bf16", [512, 333]),
+    (8101, 1, 200, 1, 2, 64, 32, "f32", None),
+    (8102, 3, 64, 2, 2, 32, 32, "bf16", [64, 0, 9]),   # no workspace below 129 slots
+]
+
+
+def test_noalloc_matches_verify(G, orc):
+    import torch
+    for seed, B, T, Hk, Hv, dk, dv, dt_, nv in CALLS:
+        print(f"[gpu] noalloc B={B} T={T} Hk={Hk} Hv={Hv} dk={dk} dv={dv} {dt_}", flush=True)
+        w = W.make_random(seed, B, T, Hk, Hv, dk, dv, dt_, n_valid=nv, shuffle=True)
+        dt = G.DeviceTree(w)
+        dt.prepare()
+        out_a, full_a = guarded(tuple(dt.out.shape))
+        out_b, full_b = guarded(tuple(dt.out.shape))
+        dt.verify(out=out_a)
+        dt.verify(out=out_b, noalloc=True)
+        torch.cuda.synchronize()
+        check_guards(full_a, "out (verify)")
+        check_guards(full_b, "out (verify_noalloc)")
+        assert torch.equal(out_a.view(torch.int32), out_b.view(torch.int32))
+        ref = orc.verify(w)
+        got = out_b.cpu().numpy().astype(np.float64)
+        err = np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30)
+        print(f"[gpu]   err vs oracle {err:.3e}", flush=True)
+        assert err <= O_TOL
+
+
+def test_noalloc_refuses_oversize(G):
+    L = G.lib()
+    d = G.make_dims(8, 512, 16, 48, 128, 128)   # 8 * 512 * 10240 * 4 bytes of features
+    assert 8 * 512 * 10240 * 4 > G.NOALLOC_SCRATCH_BYTES
+    fake = [ctypes.c_void_p(0x1000)] * 10       # never dereferenced: refused on the host
+    assert L.gdn_tree_verify_noalloc(ctypes.byref(d), *fake, None) == G.GDN_EUNSUPPORTED
+    assert "workspace" in G.last_error()
