@@ -119,6 +119,11 @@ int gdn_tree_prepare(const gdn_dims* dims, const int32_t* parent, void* meta,
                      int32_t* tree_status, hipStream_t stream);
 
 /* Read-only tree verification (Sec. 3.4: Eq. 7-8 per node along its path).
+ * Up to 128 slots everything stays on chip and nothing is allocated; above
+ * 128 the post-conv features go through a device workspace of B T C 4 bytes
+ * that the library allocates on the first call that needs it and keeps per
+ * (device, stream) until the process ends (a call under stream capture that
+ * would have to grow it returns GDN_EUNSUPPORTED).
  *   meta        written by gdn_tree_prepare for the same B, T
  *   q, k        in_dtype [B][T][Hk][dk]   raw (pre-conv) queries / keys
  *   v           in_dtype [B][T][Hv][dv]   raw values
@@ -150,18 +155,18 @@ int gdn_tree_verify_noalloc(const gdn_dims* dims, const void* meta, const void* 
                             const float* conv_w, const float* conv_state, const float* S0,
                             float* out, hipStream_t stream);
 
-/* The same verification in the paper's chunked form (Sec. 3.4.1, Eq. 9-13):
- * per (sequence, value head) the interaction matrices X (strict ancestors,
- * decayed key-key products scaled by beta) and Y (ancestors and self, decayed
- * query-key products) are built from Gram products, (I + X) U = beta (V -
- * a K S0^T) is solved by forward substitution over 16-node blocks (each
- * diagonal block inverted, the off-diagonal blocks applied as a cascade),
- * and O = scale (a Q S0^T + Y U).  All dense products run on MFMA with a
- * bf16 hi/lo split (fp32 accumulation).  Arguments, layouts, outputs and
- * errors are those of gdn_tree_verify; in addition dk and dv must be 32, 64
- * or 128 (GDN_EUNSUPPORTED otherwise).  Its cost does not grow with the
- * depth of the tree, while gdn_tree_verify's grows with the sum of the path
- * lengths. */
+/* The same verification in the paper's chunked form (Sec. 3.4.1-3.4.2,
+ * Eq. 9-13): per (sequence, value head) the interaction matrices X (strict
+ * ancestors: decayed key-key products scaled by beta) and Y (ancestors and
+ * self: decayed query-key products) are built from Gram products, (I + X) U =
+ * beta (V - a K S0^T) is solved by forward substitution over sub-blocks of 32
+ * positions (each diagonal block inverted by repeated squaring), and O =
+ * scale (a Q S0^T + Y U); every dense product on fp32 MFMA.  Arguments,
+ * layouts, outputs and errors are those of gdn_tree_verify (any supported
+ * dk, dv and T).  Needs a workspace of B T (C + Hv dv) 4 bytes, cached per
+ * (device, stream) like gdn_tree_verify's above 128 slots.  Its cost does not
+ * grow with the depth of the tree, while gdn_tree_verify's grows with the sum
+ * of the path lengths. */
 int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* q, const void* k,
                             const void* v, const void* alpha, const void* beta,
                             const float* conv_w, const float* conv_state, const float* S0,

@@ -167,7 +167,10 @@ int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* 
   a.conv_state = conv_state;
   a.S0 = S0;
   a.out = out;
-  return launch_verify_chunked(a, stream);
+  const size_t bytes = chunked_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv);
+  void* ws = stream_workspace(bytes, stream, &rc);
+  if (!ws) return rc;
+  return launch_verify_chunked(a, ws, bytes, stream);
 }
 
 int gdn_tree_commit(const gdn_dims* dims, const void* meta, const int32_t* accepted,

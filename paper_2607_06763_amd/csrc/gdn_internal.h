@@ -357,8 +357,13 @@ void* stream_workspace(size_t bytes, hipStream_t stream, int* rc);
 // gdn_tree_verify without any allocation: the workspace of T > 128 is the
 // library's static device array
 int launch_verify_noalloc(const VerifyArgs& a, hipStream_t stream);
-// the paper's chunked form (Eq. 9-13) of the same verification
-int launch_verify_chunked(const VerifyArgs& a, hipStream_t stream);
+// post-conv features of every position into F[B][T][C] (fp32, canonical
+// position order; large_workspace_bytes(...) bytes)
+int launch_features(const VerifyArgs& a, float* F, hipStream_t stream);
+// the paper's chunked form (Eq. 9-13) of the same verification; ws holds
+// chunked_workspace_bytes(...) bytes
+size_t chunked_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv);
+int launch_verify_chunked(const VerifyArgs& a, void* ws, size_t ws_bytes, hipStream_t stream);
 
 struct CommitArgs {
   int B, T, Hk, Hv, dk, dv, in_dtype;

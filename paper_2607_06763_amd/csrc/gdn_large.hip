@@ -302,8 +302,6 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 // ---------------------------------------------------------------------------
 template <int DK, int DV, typename TIn>
 static int launch_large_t(const LargeParams& p, hipStream_t stream) {
-  const int C = 2 * p.Hk * DK + p.Hv * DV;
-  (void)C;
   hipLaunchKernelGGL((feat_kernel<TIn, DK>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, DV);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
@@ -343,10 +341,7 @@ static int large_dk(const VerifyArgs& a, const LargeParams& p, hipStream_t s) {
   return set_error(GDN_EUNSUPPORTED, "verify: dk=%d unsupported", a.dk);
 }
 
-int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStream_t stream) {
-  if (a.T > kLMaxT) return set_error(GDN_EUNSUPPORTED, "verify: T=%d exceeds %d", a.T, kLMaxT);
-  if (ws_bytes < large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv))
-    return set_error(GDN_EINVAL, "verify: workspace of %zu bytes is too small", ws_bytes);
+static LargeParams large_params(const VerifyArgs& a, float* ws) {
   LargeParams p;
   p.B = a.B;
   p.T = a.T;
@@ -364,8 +359,37 @@ int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStre
   p.S0 = a.S0;
   p.out = a.out;
   p.F = ws;
+  return p;
+}
+
+int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStream_t stream) {
+  if (a.T > kLMaxT) return set_error(GDN_EUNSUPPORTED, "verify: T=%d exceeds %d", a.T, kLMaxT);
+  if (ws_bytes < large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv))
+    return set_error(GDN_EINVAL, "verify: workspace of %zu bytes is too small", ws_bytes);
+  const LargeParams p = large_params(a, ws);
   if (a.in_dtype == GDN_BF16) return large_dk<BF16>(a, p, stream);
   return large_dk<float>(a, p, stream);
+}
+
+template <typename TIn>
+static int launch_features_t(const VerifyArgs& a, const LargeParams& p, hipStream_t stream) {
+  switch (a.dk) {
+    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
+    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
+    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
+    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
+    default: return set_error(GDN_EUNSUPPORTED, "features: dk=%d unsupported", a.dk);
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(GDN_EHIP, "feature launch: %s", hipGetErrorString(e));
+  return GDN_OK;
+}
+
+int launch_features(const VerifyArgs& a, float* F, hipStream_t stream) {
+  if (a.T > kLMaxT) return set_error(GDN_EUNSUPPORTED, "features: T=%d exceeds %d", a.T, kLMaxT);
+  const LargeParams p = large_params(a, F);
+  if (a.in_dtype == GDN_BF16) return launch_features_t<BF16>(a, p, stream);
+  return launch_features_t<float>(a, p, stream);
 }
 
 // ---------------------------------------------------------------------------

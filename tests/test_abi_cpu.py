@@ -118,13 +118,13 @@ def test_step_host_validation(L):
 
 
 def test_chunked_host_validation(L):
-    d = G.make_dims(1, 7, 2, 2, 16, 16, "f32")
-    p = [ctypes.c_void_p(0x1000)] * 10
-    # head dims outside {32, 64, 128} are refused before any device work
-    assert L.gdn_tree_verify_chunked(ctypes.byref(d), *p, None) == G.GDN_EUNSUPPORTED
-    assert "dk=16" in G.last_error()
-    d2 = G.make_dims(1, 7, 2, 2, 32, 16, "f32")
-    assert L.gdn_tree_verify_chunked(ctypes.byref(d2), *p, None) == G.GDN_EUNSUPPORTED
+    p = [ctypes.c_void_p(0x1000)] * 10   # never dereferenced: refused on the host
+    # trees above GDN_MAX_T and unsupported head dims are refused before any device work
+    assert L.gdn_tree_verify_chunked(ctypes.byref(G.make_dims(1, 513, 2, 2, 32, 32)), *p,
+                                     None) == G.GDN_EUNSUPPORTED
+    assert L.gdn_tree_verify_chunked(ctypes.byref(G.make_dims(1, 7, 2, 2, 48, 32)), *p,
+                                     None) == G.GDN_EUNSUPPORTED
+    d2 = G.make_dims(1, 7, 2, 2, 16, 16, "f32")
     assert L.gdn_tree_verify_chunked(ctypes.byref(d2), *([None] * 10), None) == G.GDN_EINVAL
     assert L.gdn_tree_verify_chunked(ctypes.byref(G.make_dims(0, 7, 2, 2, 32, 32)), *([None] * 10),
                                      None) == G.GDN_OK

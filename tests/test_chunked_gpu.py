@@ -1,5 +1,7 @@
 """GPU parity of the chunked-form verification (gdn_tree_verify_chunked,
-Sec. 3.4.1 Eq. 9-13) against the CPU oracle.
+Sec. 3.4.1-3.4.2 Eq. 9-13: sub-blocks of 32 positions, diagonal blocks
+inverted by repeated squaring) against the CPU oracle, for trees of 1..512
+slots.
 
 Bars: max|o - o_ref| <= 2e-3 max|o_ref|; invalid trees and padding slots give
 zero rows; S0 and the conv state stay bit-identical."""
@@ -40,7 +42,7 @@ def _run(G, w, chunked=True):
     return dt, dt.out.cpu().numpy().astype(np.float64)
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3])
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
 def test_chunked_named_full(G, orc, cfg):
     w = W.make_config(cfg)
     _announce(f"chunked cfg={cfg} B={w.B} T={w.T}")
@@ -59,15 +61,6 @@ def test_chunked_large_full(G, orc):
     assert err <= O_TOL
 
 
-def test_chunked_unsupported_head_dim(G):
-    w = W.make_config(0)   # dk = dv = 16
-    dt = G.DeviceTree(w)
-    dt.prepare()
-    with pytest.raises(G.GdnError) as ei:
-        dt.verify(chunked=True)
-    assert ei.value.code == G.GDN_EUNSUPPORTED
-
-
 SHAPES = [
     # (B, T, Hk, Hv, dk, dv, dtype, n_valid or None, max_depth)
     (2, 1, 1, 1, 32, 32, "f32", None, None),           # one node
@@ -78,6 +71,11 @@ SHAPES = [
     (2, 128, 1, 2, 128, 128, "bf16", [128, 97], None),
     (4, 17, 4, 8, 64, 64, "bf16", [17, 0, 3, 16], 3),  # includes an empty tree
     (1, 128, 2, 2, 32, 128, "f32", None, None),
+    (2, 40, 1, 2, 16, 16, "f32", [40, 33], None),        # 16 x 16 heads
+    (2, 256, 2, 4, 128, 128, "bf16", [256, 200], None),
+    (3, 384, 3, 3, 16, 64, "bf16", [384, 0, 5], 12),    # includes an empty tree
+    (2, 512, 1, 2, 128, 128, "bf16", [512, 301], None),
+    (1, 500, 2, 2, 64, 32, "f32", None, None),           # ragged last block
 ]
 
 
@@ -93,11 +91,29 @@ def test_chunked_random_shapes(G, orc, idx):
     assert (got[w.parent == W.PAD] == 0).all()
 
 
-def test_chunked_deep_chain(G, orc):
-    """128-node chains (depth 127): the case the block solve is for."""
-    w = W.make_random(8100, 2, 128, 1, 2, 128, 128, "bf16", parent=np.stack([W.chain_tree(128)] * 2))
-    _announce("chunked chain T=128")
+@pytest.mark.parametrize("T", [128, 512])
+def test_chunked_deep_chain(G, orc, T):
+    """Chains (depth T - 1): the case the block solve is for; at T = 512 every
+    earlier block holds ancestors of every later one."""
+    w = W.make_random(8100 + T, 2, T, 1, 2, 128, 128, "bf16", parent=np.stack([W.chain_tree(T)] * 2))
+    _announce(f"chunked chain T={T}")
     _dt, got = _run(G, w)
+    err = _out_err(got, orc.verify(w))
+    _announce(f"  err {err:.3e}")
+    assert err <= O_TOL
+
+
+def test_chunked_tiny_alpha(G, orc):
+    """Decays of 1e-30 and exactly 0 on some nodes: the log-decay ratios stay
+    finite (log alpha floored at the smallest normal float)."""
+    w = W.make_random(8150, 2, 64, 1, 2, 32, 32, "f32", shuffle=True)
+    a = w.alpha.copy()
+    a[0, ::5, 0] = 1e-30
+    a[1, ::7, 1] = 0.0
+    w.alpha = a
+    _announce("chunked tiny alpha")
+    _dt, got = _run(G, w)
+    assert np.isfinite(got).all()
     err = _out_err(got, orc.verify(w))
     _announce(f"  err {err:.3e}")
     assert err <= O_TOL

@@ -227,6 +227,32 @@ def test_delta_write_returns_value(orc):
         np.testing.assert_allclose(S_new[0, h] @ kk, v, rtol=0, atol=1e-7)
 
 
+def test_zero_decay_forgets_the_past(orc):
+    """alpha = 0 at node j (Eq. 7): the state after j is beta_j v_j k_j^T
+    whatever came before, so the commit of j equals that rank-1 matrix and
+    the output of j is scale beta_j (k_j . q_j) v_j; tiny decays (1e-30)
+    elsewhere on the path keep everything finite."""
+    rng = np.random.default_rng(61)
+    par = W.random_tree(rng, 14, 14, shuffle=True)
+    w = _small(61, par, Hk=1, Hv=2, dk=8, dv=6)
+    a = int(w.accepted[0])
+    w.alpha[0, :, :] = 1e-30
+    w.alpha[0, a, :] = 0.0
+    feat = orc.features(w)
+    nq = w.Hk * w.dk
+    S_new, _cs, _st = orc.commit(w)
+    out = orc.verify(w)
+    scale = 1.0 / np.sqrt(w.dk)
+    for h in range(w.Hv):
+        kk = feat[0, a, nq: nq + w.dk]
+        qq = feat[0, a, :w.dk]
+        v = feat[0, a, 2 * nq + h * w.dv: 2 * nq + (h + 1) * w.dv]
+        be = _f64(w, "beta")[0, a, h]
+        np.testing.assert_allclose(S_new[0, h], be * np.outer(v, kk), rtol=0, atol=1e-14)
+        np.testing.assert_allclose(out[0, a, h], scale * be * (kk @ qq) * v, rtol=0, atol=1e-14)
+    assert np.isfinite(out).all() and np.isfinite(S_new).all()
+
+
 # ----------------------------------------------------------------------------
 # chains = sequential decoding in the stored orientation
 # ----------------------------------------------------------------------------

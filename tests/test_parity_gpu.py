@@ -300,3 +300,39 @@ def test_multi_step_resume(G, orc):
         # keep the oracle on the device's fp32 state so errors do not compound
         S_ref = S.cpu().numpy().astype(np.float64)
         cs_ref = cs.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("T", [64, 200])
+def test_tiny_alpha_verify_commit(G, orc, T):
+    """Decays of 1e-30, 1e-25 and exactly 0 along committed chains: the commit
+    replay never divides by an underflowed decay product, and outputs and
+    state stay finite and within the bars (T = 64: on-chip kernels, T = 200:
+    the workspace path)."""
+    import torch
+    par = np.stack([W.chain_tree(T)] * 2)
+    w = W.make_random(3500 + T, 2, T, 1, 2, 64, 64, "f32", parent=par)
+    a = w.alpha.copy()
+    a[0, ::3, :] = 1e-30
+    a[0, 1::3, :] = 1e-25
+    a[1, ::4, 0] = 0.0
+    w.alpha = a
+    w.accepted[:] = [T - 1, T // 2]
+    _announce(f"tiny alpha T={T}")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    dt.verify()
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    got = dt.out.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    err = _out_err(got, orc.verify(w))
+    S_ref, cs_ref, st_ref = orc.commit(w)
+    S_got = S.cpu().numpy()
+    assert np.isfinite(S_got).all()
+    serr = _state_err(S_got, S_ref)
+    _announce(f"  verify err {err:.3e}  state err {serr:.3e}")
+    assert err <= O_TOL
+    assert serr <= S_TOL
+    np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))

@@ -214,3 +214,19 @@ def test_step_multi(G, orc):
         _announce(f"  step {step}: out err {err:.3e}")
         assert err <= O_TOL
         prev_w, prev_d = w, d
+
+
+def test_step_tiny_alpha(G, orc):
+    """The fused step's commit with decays of 1e-30 and exactly 0 on the
+    accepted paths (128-node chains)."""
+    chain = np.stack([W.chain_tree(128)] * 2)
+    wp, wc = _pair(6900, 2, 128, 1, 2, 64, 64, "f32", prev_parent=chain)
+    a = wp.alpha.copy()
+    a[0, ::3, :] = 1e-30
+    a[1, ::4, 1] = 0.0
+    wp.alpha = a
+    wp.accepted[:] = [127, 90]
+    _announce("step tiny alpha")
+    got = _run_step(G, wp, wc)
+    assert np.isfinite(got["S"]).all()
+    _check(got, _reference(orc, wp, wc))
