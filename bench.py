@@ -21,7 +21,10 @@ back to back; the replay time is the step time (--no-graph: the eager time).
 
 Prints ONE JSON line on stdout: throughput in tree nodes verified per second
 per GDN layer, the roofline of the dominant kernel (the fused step, or verify
-with --unfused), and the CPU oracle's throughput on the same workload.
+with --unfused), the rate of a plain device copy on the same GPU, and the CPU
+oracle's throughput on the same workload (all host threads and one thread).
+--sweep instead prints one line with the fused, unfused and chunked step
+times over tree sizes 32..512 (large recipe) and on 128 / 512-node chains.
 """
 from __future__ import annotations
 
@@ -101,10 +104,21 @@ def measured_traffic(src_hash: str, kernel: str, workload: str):
         return None
 
 
-def cpu_baseline(w, max_seconds: float = 30.0) -> dict:
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, max_seconds: float = 20.0, one_thread_seconds: float = 8.0) -> dict:
     """The oracle (prepare + verify + commit) timed on this host's cores on
-    whole trees of the same workload; as many trees as fit the time budget,
-    estimated from the first tree."""
+    whole trees of the same workload, with all threads and with one thread;
+    as many trees as fit each time budget, estimated from the first tree."""
     import copy
 
     from oracle import oracle as orc
@@ -123,74 +137,60 @@ def cpu_baseline(w, max_seconds: float = 30.0) -> dict:
         orc.commit(s)
         return time.perf_counter() - t0
 
-    t1 = run(sub(1))
-    nb = max(1, min(w.B, int(max_seconds / max(t1, 1e-6))))
-    s = sub(nb)
-    dt = run(s) if nb > 1 else t1
-    return {"value": round(nb * w.T / dt, 2), "unit": "nodes/s", "cores": orc.num_threads(),
+    def rate(budget):
+        t1 = run(sub(1))
+        nb = max(1, min(w.B, int(budget / max(t1, 1e-6))))
+        dt = run(sub(nb)) if nb > 1 else t1
+        return nb, dt
+
+    cores = orc.num_threads()
+    nb, dt = rate(max_seconds)
+    orc.set_num_threads(1)
+    try:
+        nb1, dt1 = rate(one_thread_seconds)
+    finally:
+        orc.set_num_threads(cores)
+    return {"value": round(nb * w.T / dt, 2), "unit": "nodes/s", "cores": cores,
             "kind": "oracle",
+            "value_1thread": round(nb1 * w.T / dt1, 2),
+            "cpu_model": cpu_model(),
             "sample": f"{nb} of {w.B} trees x {w.T} nodes of the '{w.name}' workload, all "
                       f"{w.Hv} value heads; prepare+verify+commit; fp64 per-node path replay; "
-                      f"{dt:.2f} s"}
+                      f"{dt:.2f} s on {cores} threads; 1 thread: {nb1} trees in {dt1:.2f} s"}
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=4, help="workload index 0..4 (default: large)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--tree-size", type=int, default=0,
-                    help="run the large workload's recipe at this tree size T (16..128) instead of "
-                         "the --config workload")
-    ap.add_argument("--shape", default="large", choices=["large", "chain"],
-                    help="tree shape for --tree-size: the large recipe, or single paths of T nodes")
-    ap.add_argument("--no-graph", dest="graph", action="store_false",
-                    help="time eager launches only (default: after the eager pass, two steps are "
-                         "captured in a HIP graph and the replay time is the step time; per-kernel "
-                         "durations always come from the eager pass)")
-    ap.add_argument("--chunked", action="store_true",
-                    help="verify with the chunked-form kernel (Eq. 9-13) instead of the pull-back; "
-                         "implies --unfused")
-    ap.add_argument("--hot", action="store_true",
-                    help="back-to-back steps on warm caches: kernel times from eager steps, value from "
-                         "the HIP-graph replay (default: cold, a 512 MiB buffer is written before every "
-                         "step, outside its events, evicting L2 and the MALL; kernel times and value "
-                         "from those steps)")
-    ap.add_argument("--unfused", action="store_true",
-                    help="time prepare, verify and commit as three launches (default: prepare + "
-                         "the fused commit-then-verify step)")
-    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
-                    help="after timing, run 5 plain device copies of this many MiB (a known-size "
-                         "kernel for scaling HBM counters)")
-    args = ap.parse_args()
+def copy_rate_gbs(torch, mib: int = 512, reps: int = 5) -> float:
+    """Device-to-device copy rate (read + write bytes / time) of a plain
+    copy kernel on this GPU, timed with HIP events."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * 4 * n * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return gbs
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): every "
-              "(sequence, head) unit is independent and there is no multi-GPU path.",
-              file=sys.stderr)
-        return 2
 
-    import numpy as np
-    import torch
+DTYPE = "bf16-in/f32 (S0 readout: fp16 MFMA operands, rows scaled by powers of two, fp32 accumulate)"
 
-    from paper_2607_06763_amd import gdn_tree as G
-    from paper_2607_06763_amd import workloads as W
 
-    if not os.path.exists(G.LIB_PATH):
-        import __graft_entry__
-        __graft_entry__.build()
-    torch.cuda.set_device(0)
-    w = W.make_sweep(args.tree_size, shape=args.shape) if args.tree_size else W.make_config(args.config)
+def measure(G, torch, np, w, form: str, steps: int, warmup: int, cold: bool, graph: bool) -> dict:
+    """Times `steps` decode steps of workload w after `warmup` untimed ones.
+    form: "fused" (prepare + gdn_tree_step), "unfused" (prepare, verify,
+    commit) or "chunked" (prepare, chunked verify, commit).  Per-launch
+    durations come from HIP events recorded on the launch stream around each
+    entry point; with graph=True two steps are also captured in a HIP graph
+    and the replay time is the step time."""
     dt = G.DeviceTree(w, device="cuda:0")
     S = dt.S0.clone()
     cs = dt.conv_state.clone()
-    nbytes = algorithmic_bytes(w)
-
-    nodes = w.B * w.T
-    fused = not (args.unfused or args.chunked)
+    fused = form == "fused"
     # two metadata buffers and two conv-state buffers alternate between steps:
     # the fused launch reads the previous tree's metadata and conv state while
     # the current tree's are written
@@ -218,37 +218,36 @@ def main() -> int:
         dt.prepare()
         if ev is not None:
             ev[1].record()
-        dt.verify(S0=S, conv_state=cs, chunked=args.chunked)
+        dt.verify(S0=S, conv_state=cs, chunked=form == "chunked")
         if ev is not None:
             ev[2].record()
         dt.commit(S, cs)
         if ev is not None:
             ev[3].record()
 
-    cold = not args.hot
     flush = torch.empty((512 << 20) // 4, dtype=torch.float32, device="cuda:0") if cold else None
     if cold:
-        args.graph = False  # every launch of a cold run sees cold caches
+        graph = False  # every launch of a cold run sees cold caches
     if fused:
         G.prepare(dt.dims, dt.parent, metas[1], dt.tree_status)  # the "previous" tree of step 0
-    for i in range(args.warmup):
+    for i in range(warmup):
         if flush is not None:
             flush.fill_(float(i))
         step(i)
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    for i in range(steps):
         if flush is not None:
             flush.fill_(float(i))
-        step(args.warmup + i, events[i])
+        step(warmup + i, events[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
+    ms_step = (t1 - t0) * 1e3 / steps
     ms_eager = ms_step
     reps = 0
-    if args.graph:
+    if graph:
         # two consecutive steps (the metadata / conv-state buffers alternate)
         # captured once; warm-up launches on the capture stream first
         g = torch.cuda.CUDAGraph()
@@ -262,27 +261,130 @@ def main() -> int:
         with torch.cuda.graph(g):
             step(0)
             step(1)
-        for _ in range(max(1, args.warmup // 2)):
+        for _ in range(max(1, warmup // 2)):
             g.replay()
         torch.cuda.synchronize()
-        reps = max(1, (args.steps + 1) // 2)
+        reps = max(1, (steps + 1) // 2)
         t0 = time.perf_counter()
         for _ in range(reps):
             g.replay()
         torch.cuda.synchronize()
         ms_step = (time.perf_counter() - t0) * 1e3 / (2 * reps)
     per = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(nev - 1)] for e in events]) * 1e3
-    src_hash = verify_source_hash()
-    if fused:
-        us_prep, us_main = (float(x) for x in per.mean(0))
-        kname, kbytes = "step", nbytes["step"]
-    else:
-        us_prep, us_main, us_com = (float(x) for x in per.mean(0))
-        kname, kbytes = ("verify_chunked" if args.chunked else "verify"), nbytes["verify"]
-    p10, p50, p90 = (float(x) for x in np.percentile(per[:, 1], [10, 50, 90]))
+    r = {"us_prep": float(per[:, 0].mean()), "us_main": float(per[:, 1].mean()),
+         "us_main_p10_p50_p90": [float(x) for x in np.percentile(per[:, 1], [10, 50, 90])],
+         "us_commit": float(per[:, 2].mean()) if not fused else None,
+         "ms_eager": ms_eager, "reps": reps}
     if cold:  # the eager wall time includes the flushes: the kernels' own times
         ms_step = float(per.sum(1).mean()) * 1e-3
+    r["ms_step"] = ms_step
+    del dt, S, cs, metas, css, prev, flush
+    return r
+
+
+SWEEP_T = (32, 64, 128, 256, 512)
+
+
+def sweep(G, torch, np, W, args) -> dict:
+    """Pull-back (fused and unfused) and chunked step times over tree sizes on
+    the large recipe, and at T = 128 / 512 on chains (depth T - 1): the
+    crossover of the two verification forms."""
+    rows = []
+    cases = [("large", T) for T in SWEEP_T] + [("chain", 128), ("chain", 512)]
+    for shape, T in cases:
+        w = W.make_sweep(T, shape=shape)
+        nb = algorithmic_bytes(w)
+        row = {"shape": shape, "T": T, "B": w.B, "nodes": w.B * w.T}
+        for form in ("fused", "unfused", "chunked"):
+            r = measure(G, torch, np, w, form, args.steps, args.warmup, True, False)
+            main_bytes = nb["step"] if form == "fused" else nb["verify"]
+            row[form] = {"us_prepare": round(r["us_prep"], 2), "us_verify_or_step": round(r["us_main"], 2),
+                         "us_commit": None if r["us_commit"] is None else round(r["us_commit"], 2),
+                         "us_total": round(r["ms_step"] * 1e3, 2),
+                         "nodes_per_s": round(w.B * w.T / (r["ms_step"] * 1e-3), 1),
+                         "hbm_frac": round(main_bytes / (r["us_main"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+            print(f"[sweep] {shape} T={T} {form}: {row[form]}", file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
+        rows.append(row)
+        del w
+    return {"sweep": rows, "cold_caches": True, "steps": args.steps, "warmup": args.warmup}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=4, help="workload index 0..4 (default: large)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tree-size", type=int, default=0,
+                    help="run the large workload's recipe at this tree size T (16..512) instead of "
+                         "the --config workload")
+    ap.add_argument("--shape", default="large", choices=["large", "chain"],
+                    help="tree shape for --tree-size: the large recipe, or single paths of T nodes")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="time eager launches only (with --hot: after the eager pass, two steps are "
+                         "captured in a HIP graph and the replay time is the step time; per-kernel "
+                         "durations always come from the eager pass)")
+    ap.add_argument("--chunked", action="store_true",
+                    help="verify with the chunked-form kernel (Eq. 9-13) instead of the pull-back; "
+                         "implies --unfused")
+    ap.add_argument("--hot", action="store_true",
+                    help="back-to-back steps on warm caches: kernel times from eager steps, value from "
+                         "the HIP-graph replay (default: cold, a 512 MiB buffer is written before every "
+                         "step, outside its events, evicting L2 and the MALL; kernel times and value "
+                         "from those steps)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time prepare, verify and commit as three launches (default: prepare + "
+                         "the fused commit-then-verify step)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time fused, unfused and chunked steps over T in 32..512 on the large "
+                         "recipe and on chains; prints one JSON line with the table")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="after timing, run 5 plain device copies of this many MiB (a known-size "
+                         "kernel for scaling HBM counters)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {max(args.gpus, world)}): every "
+              "(sequence, head) unit is independent and there is no multi-GPU path.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2607_06763_amd import gdn_tree as G
+    from paper_2607_06763_amd import workloads as W
+
+    if not os.path.exists(G.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    torch.cuda.set_device(0)
+    if args.sweep:
+        res = sweep(G, torch, np, W, args)
+        res["copy_GBs"] = round(copy_rate_gbs(torch), 1)
+        print(json.dumps(res), flush=True)
+        return 0
+    w = W.make_sweep(args.tree_size, shape=args.shape) if args.tree_size else W.make_config(args.config)
+    nbytes = algorithmic_bytes(w)
+    nodes = w.B * w.T
+    form = "chunked" if args.chunked else ("unfused" if args.unfused else "fused")
+    fused = form == "fused"
+    cold = not args.hot
+    graph = args.graph and not cold
+    r = measure(G, torch, np, w, form, args.steps, args.warmup, cold, graph)
+    us_prep, us_main, ms_step = r["us_prep"], r["us_main"], r["ms_step"]
+    p10, p50, p90 = r["us_main_p10_p50_p90"]
+    src_hash = verify_source_hash()
+    if fused:
+        kname, kbytes = "step", nbytes["step"]
+    else:
+        kname, kbytes = ("verify_chunked" if args.chunked else "verify"), nbytes["verify"]
+        us_com = r["us_commit"]
     ach = kbytes / (us_main * 1e-6) / 1e9
+    copy_gbs = copy_rate_gbs(torch)
     traffic = measured_traffic(src_hash, kname, w.name)
     roofline = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic,
@@ -306,31 +408,36 @@ def main() -> int:
                 (nbytes["verify"] + nbytes["commit"]) / ((us_main + us_com) * 1e-6) / 1e9
                 / HBM_PEAK_GBS, 4),
         }
+    detail["copy_GBs"] = round(copy_gbs, 1)
+    detail["frac_of_copy"] = round(ach / copy_gbs, 4)
     detail["algorithmic_bytes"] = nbytes
     detail["caches"] = ("cold: 512 MiB written before every timed step (outside its events); value = nodes / "
                         "the mean of the step's kernel times" if cold else
-                        "hot: back-to-back steps" + ("; value from the HIP-graph replay" if args.graph else ""))
-    if args.graph:
-        detail["ms_per_step_eager"] = round(ms_eager, 5)
+                        "hot: back-to-back steps" + ("; value from the HIP-graph replay" if graph else ""))
+    if graph:
+        detail["ms_per_step_eager"] = round(r["ms_eager"], 5)
+    props = torch.cuda.get_device_properties(0)
+    detail["device"] = f"{props.name} ({getattr(props, 'gcnArchName', '?')}, {props.multi_processor_count} CUs)"
     detail["verify_source_sha256_16"] = src_hash
     out = {
         "metric": "tree nodes verified/s per GDN layer",
         "value": round(nodes / (ms_step * 1e-3), 1),
         "unit": "nodes/s",
         "n_gpus": 1,
-        "steps": 2 * reps if args.graph else args.steps,
+        "steps": 2 * r["reps"] if graph else args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": f"{w.name}: B={w.B} trees x T={w.T} nodes, Hk={w.Hk} Hv={w.Hv} "
                                f"dk={w.dk} dv={w.dv}, {w.in_dtype} inputs, fp32 state and output",
                    "global_batch": w.B, "seq_len": w.T, "parallelism": "none (1 GPU)",
                    "step": ("prepare + fused commit/verify" if fused else
-                            "prepare + " + ("chunked " if args.chunked else "") + "verify + commit") + (", HIP graph replay" if args.graph else ", cold caches" if cold else "")},
+                            "prepare + " + ("chunked " if args.chunked else "") + "verify + commit")
+                           + (", HIP graph replay" if graph else ", cold caches" if cold else "")},
         "roofline": roofline,
         "detail": detail,
     }

@@ -436,3 +436,13 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Threads used by the parallel loops from now on (n >= 1); a timing knob of
+ * the benchmark's CPU baseline, no effect on any result. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

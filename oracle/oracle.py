@@ -57,6 +57,11 @@ def num_threads() -> int:
     return int(lib().oracle_num_threads())
 
 
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (timing only)."""
+    lib().oracle_set_num_threads(ctypes.c_int(int(n)))
+
+
 def tree_status(parent_row: np.ndarray) -> int:
     p = np.ascontiguousarray(parent_row, dtype=np.int32)
     return int(lib().oracle_tree_status(ctypes.c_int(p.shape[0]), _p(p)))

@@ -76,27 +76,46 @@ __global__ __launch_bounds__(commit_threads(DK, DV)) void commit_state_kernel(Co
   const TIn* alpha = static_cast<const TIn*>(p.alpha);
   const TIn* beta = static_cast<const TIn*>(p.beta);
 
-  // ---- the accepted slot, then its path root..a read off its ancestor bitmask
+  // ---- first load wave: status, depths and gates of this thread's slots (raw
+  //      gates are converted only once the path is known)
+  constexpr int kSl = (kCMaxT + kCT - 1) / kCT;  // slots per thread
   const int a = p.accepted[b];
   const int tree_st = m.status[b];
+  int dep[kSl];
+  TIn alr[kSl], ber[kSl];
+#pragma unroll
+  for (int sl = 0; sl < kSl; ++sl) {
+    const int j = tid + sl * kCT;
+    const int jj = j < T ? j : T - 1;
+    dep[sl] = m.depth[size_t(b) * T + jj];
+    alr[sl] = alpha[(size_t(b) * T + jj) * Hv + h];
+    ber[sl] = beta[(size_t(b) * T + jj) * Hv + h];
+  }
   if (tree_st != GDN_TREE_OK || a < 0 || a >= T) {
     if (h == 0 && tid == 0 && p.commit_status)
       p.commit_status[b] = tree_st != GDN_TREE_OK ? tree_st : (a == -1 ? GDN_TREE_OK : GDN_TREE_BAD_ACCEPTED);
     return;
   }
-  for (int j = tid; j < T; j += kCT) s_dep[j] = m.depth[size_t(b) * T + j];
+  // ---- second load wave: the ancestor bitmask of a -> the path root..a
+  uint64_t word[kSl];
+#pragma unroll
+  for (int sl = 0; sl < kSl; ++sl) {
+    const int j = tid + sl * kCT;
+    word[sl] = m.anc[(size_t(b) * T + a) * m.W + ((j < T ? j : T - 1) >> 6)];
+    if (j < T) s_dep[j] = dep[sl];
+  }
   __syncthreads();
   const int d = s_dep[a];
   if (h == 0 && tid == 0 && p.commit_status)
     p.commit_status[b] = d < 0 ? GDN_TREE_BAD_ACCEPTED : GDN_TREE_OK;
   if (d < 0) return;  // accepted slot is padding
-  for (int j = tid; j < T; j += kCT) {
-    const uint64_t word = m.anc[(size_t(b) * T + a) * m.W + (j >> 6)];
-    if (j == a || ((word >> (j & 63)) & 1ull)) {
-      const int dj = s_dep[j];
-      s_path[dj] = j;
-      s_al[dj] = ld(alpha, (size_t(b) * T + j) * Hv + h);
-      s_be[dj] = ld(beta, (size_t(b) * T + j) * Hv + h);
+#pragma unroll
+  for (int sl = 0; sl < kSl; ++sl) {
+    const int j = tid + sl * kCT;
+    if (j < T && (j == a || ((word[sl] >> (j & 63)) & 1ull))) {
+      s_path[dep[sl]] = j;
+      s_al[dep[sl]] = to_f32(alr[sl]);
+      s_be[dep[sl]] = to_f32(ber[sl]);
     }
   }
   __syncthreads();

@@ -281,29 +281,26 @@ __device__ __forceinline__ float replay_rows(float (&sr)[R * CPT], const float (
   }
 #pragma unroll
   for (int i = 0; i < R; ++i) uu[i] = group_sum<LPR>(uu[i]) * inv;  // S_stored . k_hat
-  // c = beta (v_r - alpha S_true.k_hat), multiplied by 1 / ||k|| so that it
-  // applies to the raw key
-  const float ag = al * gamma;
-  if (ag >= 0x1p-60f) {
-    // stored frame: S_true' = ag (stored + c / ag k)
-    const float ri = __builtin_amdgcn_rcpf(ag) * inv;
+  // c = beta (v_r - alpha S_true.k_hat) times 1 / ||k|| (it applies to the
+  // raw key).  The decay product is the same in every lane of the workgroup:
+  // made visibly uniform so that the rescale below is a scalar branch.
+  const float ag = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(al * gamma)));
+  // stored frame while ag stays normal: S_true' = ag (stored + c / ag k);
+  // a tiny decay (ag < 2^-60, possibly 0) first moves the rows to the true
+  // frame, S_true' = ag stored + c k, with no division by ag
+  const bool tiny = ag < 0x1p-60f;
+  const float mult = tiny ? inv : __builtin_amdgcn_rcpf(ag) * inv;
+  if (tiny) {
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-      const float c = be * (vr[i] - ag * uu[i]) * ri;
-#pragma unroll
-      for (int e = 0; e < CPT; ++e) sr[i * CPT + e] += c * kk[e];
-    }
-    return ag;
+    for (int e = 0; e < R * CPT; ++e) sr[e] *= ag;
   }
-  // tiny decay (uniform branch): the step is taken in the true frame,
-  // S_true' = ag stored + c k, with no division by ag (which may be 0)
 #pragma unroll
   for (int i = 0; i < R; ++i) {
-    const float c = be * (vr[i] - ag * uu[i]) * inv;
+    const float c = be * (vr[i] - ag * uu[i]) * mult;
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) sr[i * CPT + e] = fmaf(ag, sr[i * CPT + e], c * kk[e]);
+    for (int e = 0; e < CPT; ++e) sr[i * CPT + e] += c * kk[e];
   }
-  return 1.0f;
+  return tiny ? 1.0f : ag;
 }
 
 // CPT floats of an LDS row (16-byte pieces when CPT % 4 == 0)
