@@ -171,3 +171,36 @@ def test_named_workload_trees(orc):
             assert (m["depth"].max(axis=1) == 16).all()
             for b in range(w.B):
                 assert np.bincount(w.parent[b][w.parent[b] >= 0]).max() <= 8
+
+
+from hypothesis import HealthCheck, given, settings  # noqa: E402
+from hypothesis import strategies as st  # noqa: E402
+
+
+@settings(max_examples=40, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.function_scoped_fixture, HealthCheck.too_slow])
+@given(T=st.integers(1, 512), frac=st.floats(0.0, 1.0), back=st.integers(1, 600), seed=st.integers(0, 2 ** 31 - 1))
+def test_property_prepare_vs_closure(orc, T, frac, back, seed):
+    """Random trees of 1..512 slots with padding: each node hangs at most
+    `back` slots behind its creation index (depths from ~log T up to a
+    chain), relabelled; the oracle's depths, order and ancestor bits equal
+    the transitive-closure brute force."""
+    rng = np.random.default_rng(seed)
+    nv = int(round(frac * T))
+    lp = [-1] + [int(rng.integers(max(0, i - back), i)) for i in range(1, nv)]
+    slots = rng.permutation(T)
+    par = np.full(T, W.PAD, np.int32)
+    for i in range(nv):
+        par[slots[i]] = -1 if lp[i] < 0 else slots[lp[i]]
+    m = orc.prepare(par[None])
+    assert m["status"][0] == 0 and m["nvalid"][0] == nv
+    R, depth, order = _closure_meta(par.tolist())
+    assert m["depth"][0].tolist() == depth.tolist()
+    assert m["order"][0].tolist() == order.tolist()
+    W_ = (T + 63) // 64
+    bits = np.zeros((T, W_ * 64), bool)
+    for w in range(W_):
+        words = m["anc"][0, :, w].astype(np.uint64)
+        for j in range(64):
+            bits[:, w * 64 + j] = ((words >> np.uint64(j)) & np.uint64(1)).astype(bool)
+    assert np.array_equal(bits[:, :T], R)

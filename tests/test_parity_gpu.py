@@ -336,3 +336,97 @@ def test_tiny_alpha_verify_commit(G, orc, T):
     assert err <= O_TOL
     assert serr <= S_TOL
     np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))
+
+
+def _wide_state(w, seed):
+    """S0 rows scaled by 2^e, e uniform in [-60, 60], one element per row
+    made 16 times larger: every row has its own binade range."""
+    rng = np.random.default_rng(seed)
+    B, H, dv, dk = w.S0.shape
+    S = w.S0.astype(np.float64) * np.exp2(rng.integers(-60, 61, size=(B, H, dv)))[..., None]
+    S[np.arange(B)[:, None, None], np.arange(H)[None, :, None], np.arange(dv)[None, None, :],
+      rng.integers(0, dk, size=(B, H, dv))] *= 16.0
+    return S.astype(np.float32)
+
+
+def _per_channel_err(got, ref):
+    """max over (sequence, head, value channel) of the channel's largest
+    error over the nodes / the channel's largest reference magnitude."""
+    num = np.max(np.abs(got - ref), axis=1)
+    den = np.maximum(np.max(np.abs(ref), axis=1), 1e-300)
+    return np.max(num / den)
+
+
+def _per_row_err(S, S_ref):
+    num = np.sqrt(((S.astype(np.float64) - S_ref) ** 2).sum(-1))
+    den = np.maximum(np.sqrt((S_ref ** 2).sum(-1)), 1e-300)
+    return np.max(num / den)
+
+
+# Per-channel bar of the wide-range tests.  The readout rounds both operands
+# of each product to fp16 (RNE, relative 2^-12 each), so a channel's error is
+# at most about 2^-11 sum_k |s_k x_k| <= 2^-11 |s| |x|, which exceeds 2e-3 of
+# the channel's own largest output when the products cancel; 1e-2 covers
+# that.  Without the row scaling, rows above the fp16 range would read as
+# inf and rows below it as 0 (errors of 100 %).
+WIDE_TOL = 1e-2
+
+
+@pytest.mark.parametrize("T", [64, 200])
+def test_wide_dynamic_range_state(G, orc, T):
+    """Rows of S0 spread over 2^-60..2^64 keep their relative accuracy: with
+    v = 0 every output channel is the S0 readout alone, and each is checked
+    against its own largest reference magnitude; each committed state row
+    within 1e-4 relative (T = 64: on-chip kernels, T = 200: the workspace
+    path)."""
+    import torch
+    w = W.make_random(3600 + T, 2, T, 2, 4, 64, 64, "f32", shuffle=True)
+    w.S0 = _wide_state(w, T)
+    w.v = np.zeros_like(w.v)
+    rows = np.abs(w.S0).max(-1)
+    assert rows.max() > 65504.0 and rows.min() < 6.1e-5   # beyond fp16 on both sides
+    _announce(f"wide dynamic range S0, T={T}")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    dt.verify()
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    got = dt.out.cpu().numpy().astype(np.float64)
+    ref = orc.verify(w)
+    err = _per_channel_err(got, ref)
+    S_ref, _cs_ref, _st = orc.commit(w)
+    serr = _per_row_err(S.cpu().numpy(), S_ref)
+    _announce(f"  per-channel out err {err:.3e}  per-row state err {serr:.3e}")
+    assert np.isfinite(got).all()
+    assert err <= WIDE_TOL
+    assert serr <= S_TOL
+
+
+def test_wide_dynamic_range_step(G, orc):
+    """The fused step converts the committed rows to fp16 with their own
+    scales before verifying: same per-channel / per-row bars."""
+    import torch
+    wp = W.make_random(3700, 2, 64, 2, 4, 64, 64, "f32", shuffle=True)
+    wc = W.make_random(3701, 2, 64, 2, 4, 64, 64, "f32", shuffle=True)
+    wc.conv_w = wp.conv_w
+    wp.S0 = _wide_state(wp, 5)
+    wp.v = np.zeros_like(wp.v)   # the commit keeps the rows' spread
+    wc.v = np.zeros_like(wc.v)
+    dp, dc = G.DeviceTree(wp), G.DeviceTree(wc)
+    dp.prepare()
+    dc.prepare()
+    S = dp.S0.clone()
+    cs_out = torch.empty_like(dp.conv_state)
+    dc.step_from(dp, S, dp.conv_state.clone(), cs_out)
+    torch.cuda.synchronize()
+    S_ref, cs_ref, _st = orc.commit(wp)
+    rows = np.abs(S_ref).max(-1)
+    assert rows.max() > 65504.0 and rows.min() < 6.1e-5
+    wc.S0, wc.conv_state = S_ref, cs_ref
+    err = _per_channel_err(dc.out.cpu().numpy().astype(np.float64), orc.verify(wc))
+    serr = _per_row_err(S.cpu().numpy(), S_ref)
+    _announce(f"wide dynamic range step: per-channel out err {err:.3e}  per-row state err {serr:.3e}")
+    assert err <= WIDE_TOL
+    assert serr <= S_TOL

@@ -1,0 +1,115 @@
+"""Property tests (hypothesis, derandomized) of the HIP path against the
+oracle over random shapes: T in [1, 512] with padding (including empty
+trees), 1-2 key heads with Hv / Hk in {1, 2, 3}, head dims 16..128 (dk and
+dv drawn separately), fp32 and bf16 inputs, shallow to chain-like trees.
+Every example checks verify and the chunked verify (2e-3 max|o_ref|), the
+commit (1e-4 relative Frobenius per head, statuses and conv state exact),
+and the fused step on a second tree."""
+import numpy as np
+import pytest
+from hypothesis import HealthCheck, example, given, settings
+from hypothesis import strategies as st
+
+from paper_2607_06763_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+O_TOL = 2e-3
+S_TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_06763_amd import gdn_tree as G
+    G.lib()
+    return G
+
+
+def _parents(rng, B, T, nv, back):
+    par = np.full((B, T), W.PAD, np.int32)
+    for b in range(B):
+        n = nv[b]
+        lp = [-1] + [int(rng.integers(max(0, i - back), i)) for i in range(1, n)]
+        slots = rng.permutation(T)
+        for i in range(n):
+            par[b, slots[i]] = -1 if lp[i] < 0 else slots[lp[i]]
+    return par
+
+
+def _err(got, ref):
+    return np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-30)
+
+
+def _serr(S, S_ref):
+    num = np.sqrt(((S.astype(np.float64) - S_ref) ** 2).sum((2, 3)))
+    den = np.sqrt((S_ref ** 2).sum((2, 3)))
+    return np.max(num / np.maximum(den, 1e-30))
+
+
+shapes = st.fixed_dictionaries({
+    "B": st.integers(1, 3), "T": st.integers(1, 512), "Hk": st.integers(1, 2), "ratio": st.integers(1, 3),
+    "dk": st.sampled_from([16, 32, 64, 128]), "dv": st.sampled_from([16, 32, 64, 128]),
+    "dtype": st.sampled_from(["f32", "bf16"]), "back": st.sampled_from([1, 2, 4, 600]),
+    "fracs": st.lists(st.floats(0.0, 1.0), min_size=3, max_size=3), "seed": st.integers(0, 2 ** 31 - 1)})
+
+
+def _ex(B, T, Hk, ratio, dk, dv, dtype, back, fracs, seed):
+    return example(s=dict(B=B, T=T, Hk=Hk, ratio=ratio, dk=dk, dv=dv, dtype=dtype, back=back, fracs=fracs,
+                          seed=seed))
+
+
+@settings(max_examples=40, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.function_scoped_fixture, HealthCheck.too_slow])
+@given(s=shapes)
+@_ex(3, 512, 2, 3, 128, 128, "bf16", 600, [1.0, 0.5, 0.0], 11)   # largest tree, an empty sequence
+@_ex(2, 129, 1, 2, 16, 128, "f32", 600, [1.0, 1.0, 1.0], 12)     # first size of the workspace path
+@_ex(1, 128, 2, 1, 128, 16, "bf16", 2, [1.0, 1.0, 1.0], 13)      # deep, last on-chip size
+@_ex(2, 1, 1, 3, 32, 64, "f32", 600, [1.0, 0.0, 1.0], 14)        # single node
+@_ex(3, 333, 2, 2, 64, 32, "bf16", 4, [0.6, 0.9, 0.3], 15)       # deep-ish, ragged blocks
+def test_property_verify_commit_step(G, orc, s):
+    import torch
+    B, T = s["B"], s["T"]
+    if s["back"] <= 4:   # deep trees: the oracle's per-node replay grows with T^2
+        T = min(T, 200)
+    rng = np.random.default_rng(s["seed"])
+    nv = [int(round(f * T)) for f in s["fracs"][:B]]
+    nv[0] = max(nv[0], 1)
+    Hk = s["Hk"]
+    Hv = Hk * s["ratio"]
+    par = _parents(rng, B, T, nv, s["back"])
+    w = W.make_random(s["seed"], B, T, Hk, Hv, s["dk"], s["dv"], s["dtype"], parent=par)
+    print(f"[gpu] property B={B} T={T} Hk={Hk} Hv={Hv} dk={s['dk']} dv={s['dv']} {s['dtype']} "
+          f"back={s['back']} nv={nv}", flush=True)
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    dt.verify()
+    out_c = torch.empty_like(dt.out)
+    dt.verify(out=out_c, chunked=True)
+    S = dt.S0.clone()
+    cs = dt.conv_state.clone()
+    dt.commit(S, cs)
+    torch.cuda.synchronize()
+    ref = orc.verify(w)
+    assert _err(dt.out.cpu().numpy().astype(np.float64), ref) <= O_TOL
+    assert _err(out_c.cpu().numpy().astype(np.float64), ref) <= O_TOL
+    S_ref, cs_ref, st_ref = orc.commit(w)
+    np.testing.assert_array_equal(dt.commit_status.cpu().numpy(), st_ref)
+    assert _serr(S.cpu().numpy(), S_ref) <= S_TOL
+    np.testing.assert_array_equal(cs.cpu().numpy(), cs_ref.astype(np.float32))
+    # fused step: commit of w's accepted node, then verify of a second tree
+    par2 = _parents(rng, B, T, [max(1, x) for x in nv], s["back"])
+    w2 = W.make_random(s["seed"] + 1, B, T, Hk, Hv, s["dk"], s["dv"], s["dtype"], parent=par2)
+    w2.conv_w = w.conv_w
+    d2 = G.DeviceTree(w2)
+    d2.prepare()
+    S2 = dt.S0.clone()
+    cs_out = torch.empty_like(cs)
+    d2.step_from(dt, S2, dt.conv_state.clone(), cs_out)
+    torch.cuda.synchronize()
+    w2.S0, w2.conv_state = S_ref, cs_ref
+    assert _err(d2.out.cpu().numpy().astype(np.float64), orc.verify(w2)) <= O_TOL
+    assert _serr(S2.cpu().numpy(), S_ref) <= S_TOL
+    np.testing.assert_array_equal(cs_out.cpu().numpy(), cs_ref.astype(np.float32))
