@@ -6,18 +6,27 @@
  * Method: "Trees from Marginals", Sec. 3.4.  Every tree node's output is the
  * gated delta rule (Eq. 7) applied along that node's own root-to-node path,
  * starting from the cached per-sequence state S0, followed by the readout of
- * Eq. 8.  Verification never writes the cache; once the accepted node is
- * known, a separate commit replays Eq. 7 along its path and writes the state
- * (Sec. 3.4.2: "the only state write").  The tree metadata (depths, a
- * topological order, proper-ancestor bitmasks) is computed once per decode
- * step from parent pointers and shared by every GDN layer (Sec. 3.4.2).
+ * Eq. 8.  Verification only reads the cached state and conv state; the
+ * state changes in one place per decode step, the commit, which runs Eq. 7
+ * over the accepted node's path once that node has been chosen (Sec. 3.4.2).
+ * The tree metadata (depths, a topological order, proper-ancestor bitmasks)
+ * is computed once per decode step from the parent pointers and can be
+ * shared by every GDN layer of the step (Sec. 3.4.2).
+ *
+ * Which entry point takes which tree size: gdn_tree_prepare, gdn_tree_commit,
+ * gdn_tree_verify, gdn_tree_verify_noalloc, gdn_tree_verify_chunked and
+ * gdn_tree_step all accept 1 <= T <= GDN_MAX_T = 512.  Up to 128 slots verify
+ * and step run entirely on chip (step as one fused launch); above 128 they
+ * go through a feature workspace (see gdn_tree_verify) and the step runs the
+ * commit and the verify as separate launches on the stream.
  *
  * Conventions shared by all entry points
  * --------------------------------------
  *  * All tensor pointers are DEVICE pointers, contiguous row-major, owned by
- *    the caller.  The library never allocates, frees or synchronises; work is
- *    enqueued on the caller's stream and is ordered with it.  Pointers must be
- *    16-byte aligned.
+ *    the caller.  Work is enqueued on the caller's stream and is ordered with
+ *    it; nothing synchronises the host except a workspace allocation (trees
+ *    above 128 slots, see gdn_tree_verify).  Pointers must be 16-byte
+ *    aligned.
  *  * Recurrence orientation: the stored state of (sequence b, value head h) is
  *    S[b][h] in R^{dv x dk} (dk contiguous), the transpose of the paper's
  *    S in R^{dk x dv}; one step is S <- alpha S (I - beta k k^T) + beta v k^T
@@ -172,8 +181,8 @@ int gdn_tree_verify_chunked(const gdn_dims* dims, const void* meta, const void* 
                             const float* conv_w, const float* conv_state, const float* S0,
                             float* out, hipStream_t stream);
 
-/* Commit of the accepted node (Sec. 3.4.2: a single pass replays Eq. 7 along
- * the accepted path and writes the state).
+/* Commit of the accepted node (Sec. 3.4.2): Eq. 7 is run over the path
+ * root..accepted, starting from S, and the result replaces S.
  *   accepted      int32 [B]  accepted slot per sequence, -1 = commit nothing
  *   q, k, v, alpha, beta, conv_w: as for verify (same step's tensors)
  *   conv_state    fp32 [B][3][C]   in/out: replaced by the last 3 raw inputs

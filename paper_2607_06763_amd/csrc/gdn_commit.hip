@@ -1,6 +1,7 @@
-// gdn_commit.hip -- commit of the accepted node (paper Sec. 3.4.2: once the
-// accepted leaf is known a single pass replays Eq. 7 along its path and
-// writes the state; it is the only state write of the decode step).
+// gdn_commit.hip -- commit of the accepted node (Sec. 3.4.2).  Verification
+// leaves the cached state untouched; after the decoder has chosen the
+// accepted slot, these kernels advance S and the conv state over the slot's
+// path root..a (Eq. 7 per path node), the one place the state changes.
 //
 // Kernel 1 (grid Hv x B, 512 threads): the path root..a of the accepted slot
 // a is read off its ancestor bitmask; one thread per (feature channel, half
@@ -13,10 +14,16 @@
 //     S_r <- alpha S_r + beta (v_r - alpha (S_r . k)) k^T,
 // which is Eq. 7 in the stored orientation S <- alpha S (I - beta k k^T) + beta v k^T.
 // The rows are kept as S = gamma * S_stored with gamma the running product of
-// alpha, so a step is two FMAs per element (dot and write).
+// alpha, so a step is two FMAs per element (dot and write); when gamma would
+// fall below 2^-60 (or alpha is 0) the rows are first rescaled to the true
+// frame, so no step divides by a vanishing decay (replay_rows).  Paths of up
+// to 512 nodes: the path is read off the bitmask (up to 8 words) in one load
+// wave, and features are built in chunks of 32 path nodes.
 // Kernel 2 (grid ceil(C/256) x B) shifts the conv state: the new slots are
 // the last three raw inputs of (old slots | path root..a).  It runs after
-// kernel 1 on the same stream because kernel 1 reads the old conv state.
+// kernel 1 on the same stream because kernel 1 reads the old conv state; it
+// may write to a separate output buffer (the step above 128 slots), which
+// then also receives the unchanged slots of sequences that commit nothing.
 #include "gdn_internal.h"
 
 namespace gdn {

@@ -1,5 +1,6 @@
-"""HIP graph capture of a decode step (Sec. 3.4.2: the tree shapes are fixed,
-so the whole pass is captured once and replayed).
+"""HIP graph capture of a decode step (Sec. 3.4.2: with fixed tree shapes the
+launches of a step do not change from step to step, so they can be recorded
+as a graph and replayed).
 
 One decode step = prepare of the current tree, the fused commit-then-verify
 launch, and the copy of the committed conv state back into the input buffer.
