@@ -8,17 +8,17 @@
 // gives o_i = scale (S0 (r x) + acc) in the stored orientation.  With up to
 // 512 slots the post-conv features of a tree no longer fit in LDS, so the
 // work is split in two launches:
-//   feat_kernel   one workgroup per (position, sequence): the width-4 conv
-//                 along the node's path (conv-state slots above the root),
-//                 SiLU, and the per-head L2 norm of q and k, for every
-//                 channel; written to a workspace F[B][T][C] (fp32, canonical
+//   feat_kernel   one workgroup per (1024 channels, 32 positions, sequence):
+//                 the width-4 conv along each node's path (conv-state slots
+//                 above the root), SiLU, and the per-head L2 norm of q and
+//                 k; written to a workspace F[B][T][C] (fp32, canonical
 //                 position order, channels as in conv_w)
 //   pull_kernel   one workgroup per (value head, sequence), 512 threads:
 //                 the head's S0 as one fp16 plane in LDS (each row scaled by
 //                 the power of two that puts its largest magnitude in [1, 2),
 //                 exact, undone on the output), then tiles of 32 positions:
 //                 16 lanes per node walk the paths with the features of the
-//                 path nodes gathered from F (one step of loads ahead),
+//                 path nodes gathered from F (two steps of loads ahead),
 //                 r x -> an fp16 tile, O^T = S0 (r X)^T on
 //                 v_mfma_f32_16x16x32_f16 (fp32 accumulation), plus acc.
 #include <map>
@@ -48,64 +48,86 @@ size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
 }
 
 // ---------------------------------------------------------------------------
-// Features of one position: conv taps along the path, SiLU, L2 norm (q, k)
+// Features: conv taps along the path, SiLU, L2 norm (q, k).  One workgroup
+// per (1024 channels, block of kFP positions, sequence): each thread keeps
+// the conv weights of its 4 channels in registers, the blocks' conv taps are
+// resolved once into LDS, and the raw rows of kFU positions are loaded
+// before any of them is used.
 // ---------------------------------------------------------------------------
+constexpr int kFP = 32;  // positions per feature workgroup
+constexpr int kFU = 4;   // positions whose loads are in flight together
+
 template <typename TIn, int DK>
 __global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
-  const int pos = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  __shared__ int s_tap[kFP][4];  // node of each tap, or -1 - conv-state slot
+  const int b = blockIdx.z, tid = threadIdx.x;
+  const int p0 = blockIdx.y * kFP;
   const int T = p.T, Hk = p.Hk, Hv = p.Hv;
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
-  if (m.status[b] != GDN_TREE_OK || pos >= m.nvalid[b]) return;  // uniform
+  const int nval = m.status[b] == GDN_TREE_OK ? m.nvalid[b] : 0;
+  if (p0 >= nval) return;  // uniform
+  const int np = nval - p0 < kFP ? nval - p0 : kFP;
   const size_t bt = size_t(b) * T;
+  if (tid < np) {
+    // the 4 taps of position p0 + tid (3 = the node itself): a path node's
+    // raw row, or the conv-state slot d + w for taps above the root
+    const int pos = p0 + tid;
+    const int d = m.pdep[bt + pos];
+    const int t2 = m.ppos[bt + pos];
+    const int t1 = t2 >= 0 ? m.ppos[bt + t2] : -1;
+    const int t0 = t1 >= 0 ? m.ppos[bt + t1] : -1;
+    const int tp[4] = {t0, t1, t2, pos};
+#pragma unroll
+    for (int w = 0; w < 4; ++w) s_tap[tid][w] = d - 3 + w >= 0 ? m.order[bt + tp[w]] : -1 - (d + w);
+  }
   const int nq = Hk * DK;
   const int C = 2 * nq + Hv * DV;
-  // the 4 taps (3 = the node itself): a path node's raw row, or the
-  // conv-state slot d + w for taps above the root
-  const int d = m.pdep[bt + pos];
-  const int t2 = m.ppos[bt + pos];
-  const int t1 = t2 >= 0 ? m.ppos[bt + t2] : -1;
-  const int t0 = t1 >= 0 ? m.ppos[bt + t1] : -1;
-  const int tp[4] = {t0, t1, t2, pos};
-  int node[4];
+  const int c4 = blockIdx.x * kFT + tid;
+  const bool ok = c4 < C / 4;
+  const int c = ok ? 4 * c4 : 0;
+  // this thread's channels: source tensor, row stride and offset
+  const TIn* src;
+  size_t stride;
+  int off;
+  if (c < nq) {
+    src = static_cast<const TIn*>(p.q), stride = nq, off = c;
+  } else if (c < 2 * nq) {
+    src = static_cast<const TIn*>(p.k), stride = nq, off = c - nq;
+  } else {
+    src = static_cast<const TIn*>(p.v), stride = size_t(Hv) * DV, off = c - 2 * nq;
+  }
+  src += bt * stride + off;
+  const float* cs = p.conv_state + size_t(b) * 3 * C + c;
+  const float4* wr = reinterpret_cast<const float4*>(p.conv_w + size_t(c) * 4);
+  const float4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
+  const bool qk = c < 2 * nq;
+  float* dst = p.F + (bt + p0) * size_t(C) + c;
+  __syncthreads();
+  for (int i0 = 0; i0 < np; i0 += kFU) {
+    float4 x[kFU][4];
 #pragma unroll
-  for (int w = 0; w < 4; ++w) node[w] = d - 3 + w >= 0 ? m.order[bt + tp[w]] : -1 - (d + w);
-  const TIn* q = static_cast<const TIn*>(p.q);
-  const TIn* k = static_cast<const TIn*>(p.k);
-  const TIn* v = static_cast<const TIn*>(p.v);
-  const float* cs = p.conv_state + size_t(b) * 3 * C;
-  float* dst = p.F + (bt + pos) * size_t(C);
-  const int n4 = C / 4;
-  // uniform trip count: every lane takes part in the group sums
-  for (int it = 0; it < (n4 + kFT - 1) / kFT; ++it) {
-    const int c4 = it * kFT + tid;
-    const bool ok = c4 < n4;
-    const int c = ok ? 4 * c4 : 0;
-    float4 x[4];
+    for (int u = 0; u < kFU; ++u) {
+      const int i = i0 + u < np ? i0 + u : np - 1;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const int nd = node[w];
-      if (nd < 0) {
-        x[w] = ld4(cs + size_t(-1 - nd) * C + c);
-      } else if (c < nq) {
-        x[w] = ld4(q + (bt + nd) * nq + c);
-      } else if (c < 2 * nq) {
-        x[w] = ld4(k + (bt + nd) * nq + (c - nq));
-      } else {
-        x[w] = ld4(v + (bt + nd) * size_t(Hv) * DV + (c - 2 * nq));
+      for (int w = 0; w < 4; ++w) {
+        const int nd = s_tap[i][w];
+        x[u][w] = nd >= 0 ? ld4(src + size_t(nd) * stride) : ld4(cs + size_t(-1 - nd) * C);
       }
     }
-    const float4* wr = reinterpret_cast<const float4*>(p.conv_w + size_t(c) * 4);
-    const float4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
-    float y[4];
-    y[0] = silu(fmaf(w0.w, x[3].x, fmaf(w0.z, x[2].x, fmaf(w0.y, x[1].x, w0.x * x[0].x))));
-    y[1] = silu(fmaf(w1.w, x[3].y, fmaf(w1.z, x[2].y, fmaf(w1.y, x[1].y, w1.x * x[0].y))));
-    y[2] = silu(fmaf(w2.w, x[3].z, fmaf(w2.z, x[2].z, fmaf(w2.y, x[1].z, w2.x * x[0].z))));
-    y[3] = silu(fmaf(w3.w, x[3].w, fmaf(w3.z, x[2].w, fmaf(w3.y, x[1].w, w3.x * x[0].w))));
-    // the DK / 4 lanes of a q or k head are consecutive lanes of one wave
-    float ss = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
-    ss = group_sum<DK / 4>(ss);
-    const float f = c < 2 * nq ? rsqrt_hw(ss + 1e-6f) : 1.0f;
-    if (ok) *reinterpret_cast<float4*>(dst + c) = make_float4(y[0] * f, y[1] * f, y[2] * f, y[3] * f);
+#pragma unroll
+    for (int u = 0; u < kFU; ++u) {
+      float y[4];
+      y[0] = silu(fmaf(w0.w, x[u][3].x, fmaf(w0.z, x[u][2].x, fmaf(w0.y, x[u][1].x, w0.x * x[u][0].x))));
+      y[1] = silu(fmaf(w1.w, x[u][3].y, fmaf(w1.z, x[u][2].y, fmaf(w1.y, x[u][1].y, w1.x * x[u][0].y))));
+      y[2] = silu(fmaf(w2.w, x[u][3].z, fmaf(w2.z, x[u][2].z, fmaf(w2.y, x[u][1].z, w2.x * x[u][0].z))));
+      y[3] = silu(fmaf(w3.w, x[u][3].w, fmaf(w3.z, x[u][2].w, fmaf(w3.y, x[u][1].w, w3.x * x[u][0].w))));
+      // the DK / 4 lanes of a q or k head are consecutive lanes of one wave
+      float ss = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
+      ss = group_sum<DK / 4>(ss);
+      const float f = qk ? rsqrt_hw(ss + 1e-6f) : 1.0f;
+      if (ok && i0 + u < np)
+        *reinterpret_cast<float4*>(dst + size_t(i0 + u) * C) = make_float4(y[0] * f, y[1] * f, y[2] * f, y[3] * f);
+    }
   }
 }
 
@@ -221,22 +243,26 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
     for (int e = 0; e < CK; ++e) x[e] = 0.0f;
     if (real) {
       ld_f<CK>(Fb + size_t(pos) * C + g * DK + ln * CK, x);
-      // walk to the root; the path node's features load one step ahead
+      // walk to the root; the path nodes' features load two steps ahead
+      const float* Fk = Fb + nq + g * DK + ln * CK;
+      const float* Fv = Fb + 2 * nq + h * DV + ln * CV;
       int t = pos;
-      float kc[CK], vc[CV];
-      ld_f<CK>(Fb + size_t(t) * C + nq + g * DK + ln * CK, kc);
-      ld_f<CV>(Fb + size_t(t) * C + 2 * nq + h * DV + ln * CV, vc);
+      int t1 = s_ppos[t];
+      int t2 = t1 >= 0 ? s_ppos[t1] : -1;
+      float kc[CK], vc[CV], k1[CK], v1[CV];
+      ld_f<CK>(Fk + size_t(t) * C, kc);
+      ld_f<CV>(Fv + size_t(t) * C, vc);
+      {
+        const size_t o1 = size_t(t1 >= 0 ? t1 : t) * C;  // clamped: not used past the root
+        ld_f<CK>(Fk + o1, k1);
+        ld_f<CV>(Fv + o1, v1);
+      }
       while (t >= 0) {  // uniform per 16-lane node group
-        const int tn = s_ppos[t];
-        float kn[CK], vn[CV];
-        if (tn >= 0) {
-          ld_f<CK>(Fb + size_t(tn) * C + nq + g * DK + ln * CK, kn);
-          ld_f<CV>(Fb + size_t(tn) * C + 2 * nq + h * DV + ln * CV, vn);
-        } else {
-#pragma unroll
-          for (int e = 0; e < CK; ++e) kn[e] = 0.0f;
-#pragma unroll
-          for (int e = 0; e < CV; ++e) vn[e] = 0.0f;
+        float k2[CK], v2[CV];
+        {
+          const size_t o2 = size_t(t2 >= 0 ? t2 : t) * C;
+          ld_f<CK>(Fk + o2, k2);
+          ld_f<CV>(Fv + o2, v2);
         }
         float s = 0.0f;
 #pragma unroll
@@ -249,11 +275,19 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 #pragma unroll
         for (int e = 0; e < CK; ++e) x[e] = fmaf(-c, kc[e], x[e]);
         r *= s_al[t];
-        t = tn;
+        t = t1;
+        t1 = t2;
+        t2 = t2 >= 0 ? s_ppos[t2] : -1;
 #pragma unroll
-        for (int e = 0; e < CK; ++e) kc[e] = kn[e];
+        for (int e = 0; e < CK; ++e) {
+          kc[e] = k1[e];
+          k1[e] = k2[e];
+        }
 #pragma unroll
-        for (int e = 0; e < CV; ++e) vc[e] = vn[e];
+        for (int e = 0; e < CV; ++e) {
+          vc[e] = v1[e];
+          v1[e] = v2[e];
+        }
       }
     }
     // r x -> fp16 tile row jn (zero for padding positions)
@@ -300,9 +334,14 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 // ---------------------------------------------------------------------------
 // Launch
 // ---------------------------------------------------------------------------
+static dim3 feat_grid(const LargeParams& p, int dk, int dv) {
+  const int n4 = (2 * p.Hk * dk + p.Hv * dv) / 4;
+  return dim3((n4 + kFT - 1) / kFT, (p.T + kFP - 1) / kFP, p.B);
+}
+
 template <int DK, int DV, typename TIn>
 static int launch_large_t(const LargeParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((feat_kernel<TIn, DK>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, DV);
+  hipLaunchKernelGGL((feat_kernel<TIn, DK>), feat_grid(p, DK, DV), dim3(kFT), 0, stream, p, DV);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
   using SM = PullSmem<DK, DV>;
@@ -374,10 +413,10 @@ int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStre
 template <typename TIn>
 static int launch_features_t(const VerifyArgs& a, const LargeParams& p, hipStream_t stream) {
   switch (a.dk) {
-    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
-    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
-    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
-    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128>), dim3(p.T, p.B), dim3(kFT), 0, stream, p, a.dv); break;
+    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16>), feat_grid(p, 16, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
+    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32>), feat_grid(p, 32, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
+    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64>), feat_grid(p, 64, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
+    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128>), feat_grid(p, 128, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
     default: return set_error(GDN_EUNSUPPORTED, "features: dk=%d unsupported", a.dk);
   }
   const hipError_t e = hipGetLastError();
