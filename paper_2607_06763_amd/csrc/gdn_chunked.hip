@@ -18,9 +18,12 @@
 //
 // The features come from the feature kernel (gdn_large.hip) in a workspace
 // F[B][T][C]; U[B][Hv][T][dv] is a second workspace.  One workgroup per
-// (value head, sequence), 512 threads = 8 waves; every product is a set of
-// 16 x 16 tiles on v_mfma_f32_16x16x4f32 (fp32 operands, fp32 accumulation)
-// with operands in LDS:
+// (value head, sequence), 512 threads = 8 waves; products are 16 x 16 MFMA
+// tiles with operands in LDS.  The large ones (the S0 products, the Gram
+// blocks and the block updates) take both operands as bf16 hi/lo planes and
+// three v_mfma_f32_16x16x32_bf16 (hi*hi + hi*lo + lo*hi, fp32 accumulation,
+// ~1e-5 relative); the diagonal-block inverse and its two products stay on
+// v_mfma_f32_16x16x4f32 (fp32 operands):
 //   phase A  S0 staged once; for each block: a Q S0^T -> out (node order),
 //            beta (V - a K S0^T) -> U (padding rows zero)
 //   phase B  for each block j in order: R_j, O_j in registers; for every
@@ -55,10 +58,18 @@ struct ChunkParams {
 
 template <int DK, int DV>
 struct ChunkSmem {
-  static constexpr int LK = DK + 4, LV = DV + 4;
-  static constexpr size_t head = size_t(2) * kBc * LK * 4;  // block queries and keys
-  static constexpr size_t uni_a = size_t(DV) * LK * 4;      // phase A: S0
-  static constexpr size_t uni_b = size_t(kBc) * LK * 4 + size_t(2) * kBc * LV * 4 + size_t(6) * kBc * kLs * 4;
+  static constexpr int KP = DK < 32 ? 32 : DK;  // contraction extent of the key products (zero padded)
+  static constexpr int LKH = KP + 8;            // bf16 plane row (halves)
+  static constexpr int LV = DV + 4;             // fp32 row of a 32 x DV block
+  static constexpr int UL = kBc + 8;            // bf16 row of a 32-column plane (X, Y, transposed U)
+  static constexpr size_t pk = size_t(kBc) * LKH * 2;  // one 32-row key plane
+  static constexpr size_t head = 4 * pk;               // block q and k planes (hi, lo)
+  static constexpr size_t uni_a = size_t(2) * DV * LKH * 2;  // phase A: S0 planes
+  static constexpr size_t uni_b = 2 * pk                     // keys of block c
+                                  + size_t(2) * DV * UL * 2  // U of block c, transposed
+                                  + size_t(4) * kBc * UL * 2  // -X and Y blocks
+                                  + size_t(5) * kBc * kLs * 4  // Y_jj, powers, partial products
+                                  + size_t(2) * kBc * LV * 4;  // R_j, U_j
   static constexpr size_t uni = uni_a > uni_b ? uni_a : uni_b;
   static constexpr size_t anc = size_t(kBc) * kHW * 8;
   static constexpr size_t meta = size_t(kHMaxT) * (2 + 2 + 4 + 4 + 4);
@@ -98,25 +109,67 @@ __device__ __forceinline__ void st_tile(float* m, int ti, int tj, int lane, f32x
   for (int r = 0; r < 4; ++r) m[(16 * ti + 4 * (lane >> 4) + r) * kLs + 16 * tj + (lane & 15)] = v[r];
 }
 
+// x -> bf16 hi (truncation) + bf16 lo (truncation of the remainder)
+__device__ __forceinline__ uint32_t hi16(float x) { return __float_as_uint(x) >> 16; }
+__device__ __forceinline__ uint32_t lo16(float x) {
+  return __float_as_uint(x - __uint_as_float(__float_as_uint(x) & 0xffff0000u)) >> 16;
+}
+// 4 consecutive floats -> hi / lo planes (8 bytes each)
+__device__ __forceinline__ void st_split4(uint16_t* hi, uint16_t* lo, float4 v) {
+  *reinterpret_cast<uint2*>(hi) = make_uint2(hi16(v.x) | (hi16(v.y) << 16), hi16(v.z) | (hi16(v.w) << 16));
+  *reinterpret_cast<uint2*>(lo) = make_uint2(lo16(v.x) | (lo16(v.y) << 16), lo16(v.z) | (lo16(v.w) << 16));
+}
+__device__ __forceinline__ void st_split1(uint16_t* hi, uint16_t* lo, float x) {
+  *hi = uint16_t(hi16(x));
+  *lo = uint16_t(lo16(x));
+}
+
+// acc += A (16 x K) B (K x 16) for one 16 x 16 tile from bf16 hi/lo planes:
+// A[i][k] = a[i * lda + k], B[k][j] = b[j * ldb + k] (k contiguous in both);
+// three v_mfma_f32_16x16x32_bf16 per 32 k.
+template <int K>
+__device__ __forceinline__ f32x4 mm16x3(const uint16_t* ah, const uint16_t* al, int lda, const uint16_t* bh,
+                                        const uint16_t* bl, int ldb, f32x4 acc, int lane) {
+  const int i = lane & 15, kk = 8 * (lane >> 4);
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += 32) {
+    const bf16x8 xah = *reinterpret_cast<const bf16x8*>(ah + i * lda + k0 + kk);
+    const bf16x8 xal = *reinterpret_cast<const bf16x8*>(al + i * lda + k0 + kk);
+    const bf16x8 xbh = *reinterpret_cast<const bf16x8*>(bh + i * ldb + k0 + kk);
+    const bf16x8 xbl = *reinterpret_cast<const bf16x8*>(bl + i * ldb + k0 + kk);
+    acc = mfma3(xah, xal, xbh, xbl, acc);
+  }
+  return acc;
+}
+
 template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   using SM = ChunkSmem<DK, DV>;
-  constexpr int LK = SM::LK, LV = SM::LV;
+  constexpr int KP = SM::KP, LKH = SM::LKH, LV = SM::LV, UL = SM::UL;
   constexpr int NTV = DV / 16;    // tiles across dv
   constexpr int NTILE = 2 * NTV;  // tiles of a 32 x DV block matrix
   extern __shared__ __align__(16) unsigned char smem[];
-  float* s_q = reinterpret_cast<float*>(smem);  // [32][LK]
-  float* s_k = s_q + kBc * LK;                  // [32][LK]
-  float* s_s0 = s_k + kBc * LK;                 // phase A: [DV][LK]
-  float* s_kc = s_s0;                           // phase B: keys of block c [32][LK]
-  float* s_uc = s_kc + kBc * LK;                // rows of U [32][LV]
-  float* s_rt = s_uc + kBc * LV;                // R_j [32][LV]
-  float* s_x = s_rt + kBc * LV;                 // -X blocks [32][kLs]
-  float* s_y = s_x + kBc * kLs;                 // Y blocks
-  float* s_pa = s_y + kBc * kLs;                // powers of A
+  uint16_t* s_qh = reinterpret_cast<uint16_t*>(smem);  // block q~ planes [32][LKH]
+  uint16_t* s_ql = s_qh + kBc * LKH;
+  uint16_t* s_kh = s_ql + kBc * LKH;                    // block k~ planes
+  uint16_t* s_kl = s_kh + kBc * LKH;
+  uint16_t* s_s0h = reinterpret_cast<uint16_t*>(smem + SM::head);  // phase A: S0 planes [DV][LKH]
+  uint16_t* s_s0l = s_s0h + DV * LKH;
+  uint16_t* s_kch = reinterpret_cast<uint16_t*>(smem + SM::head);  // phase B: keys of block c
+  uint16_t* s_kcl = s_kch + kBc * LKH;
+  uint16_t* s_uth = s_kcl + kBc * LKH;  // U of block c, transposed [DV][UL]
+  uint16_t* s_utl = s_uth + DV * UL;
+  uint16_t* s_xh = s_utl + DV * UL;     // -X_jc [32][UL]
+  uint16_t* s_xl = s_xh + kBc * UL;
+  uint16_t* s_yh = s_xl + kBc * UL;     // Y_jc
+  uint16_t* s_yl = s_yh + kBc * UL;
+  float* s_y = reinterpret_cast<float*>(s_yl + kBc * UL);  // Y_jj [32][kLs] (fp32)
+  float* s_pa = s_y + kBc * kLs;                            // powers of A
   float* s_pb = s_pa + kBc * kLs;
-  float* s_ma = s_pb + kBc * kLs;               // partial products of the inverse
+  float* s_ma = s_pb + kBc * kLs;                           // partial products of the inverse
   float* s_mb = s_ma + kBc * kLs;
+  float* s_rt = s_mb + kBc * kLs;                           // R_j [32][LV]
+  float* s_uj = s_rt + kBc * LV;                            // U_j [32][LV]
   uint64_t* s_anc = reinterpret_cast<uint64_t*>(smem + SM::head + SM::uni);  // [32][kHW]
   int16_t* s_ord = reinterpret_cast<int16_t*>(s_anc + kBc * kHW);
   int16_t* s_ppos = s_ord + kHMaxT;
@@ -162,13 +215,25 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
     const float* S0 = p.S0 + (size_t(b) * Hv + h) * size_t(DV) * DK;
     for (int i = tid; i < DV * DK / 4; i += kHT) {
       const int r = i / (DK / 4), c4 = i % (DK / 4);
-      *reinterpret_cast<float4*>(s_s0 + r * LK + 4 * c4) = *reinterpret_cast<const float4*>(S0 + size_t(r) * DK + 4 * c4);
+      st_split4(s_s0h + r * LKH + 4 * c4, s_s0l + r * LKH + 4 * c4,
+                *reinterpret_cast<const float4*>(S0 + size_t(r) * DK + 4 * c4));
+    }
+    if constexpr (DK < KP) {  // zero padding of the contraction
+      for (int i = tid; i < DV * (KP - DK); i += kHT) {
+        const int r = i / (KP - DK), c = DK + i % (KP - DK);
+        s_s0h[r * LKH + c] = 0;
+        s_s0l[r * LKH + c] = 0;
+      }
+      for (int i = tid; i < 4 * kBc * (KP - DK); i += kHT) {
+        const int r = i / (KP - DK), c = DK + i % (KP - DK);
+        s_qh[r * LKH + c] = 0;  // q and k planes are contiguous: rows 0 .. 4 kBc - 1
+      }
     }
   }
   __syncthreads();
 
   const int NB = (T + kBc - 1) / kBc, NBv = (nval + kBc - 1) / kBc;
-  // block rows of q~ and k~ (zero past the tree) -> s_q, s_k
+  // block rows of q~ and k~ (zero past the tree) -> hi / lo planes
   auto load_qk = [&](int jb) {
     for (int i = tid; i < 2 * kBc * (DK / 4); i += kHT) {
       const int part = i / (kBc * (DK / 4)), rem = i % (kBc * (DK / 4));
@@ -176,7 +241,7 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
       const int pos = kBc * jb + r;
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (pos < nval) v = *reinterpret_cast<const float4*>(Fb + pos * C + (part ? nq : 0) + g * DK + 4 * c4);
-      *reinterpret_cast<float4*>((part ? s_k : s_q) + r * LK + 4 * c4) = v;
+      st_split4((part ? s_kh : s_qh) + r * LKH + 4 * c4, (part ? s_kl : s_ql) + r * LKH + 4 * c4, v);
     }
   };
 
@@ -188,7 +253,8 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
       for (int task = wave; task < 2 * NTILE; task += kHT / 64) {
         const int kind = task / NTILE, t = task % NTILE;
         const int ti = t / NTV, tj = t % NTV;
-        const f32x4 acc = mm16<DK, true>((kind ? s_k : s_q) + 16 * ti * LK, LK, s_s0 + 16 * tj * LK, LK, zero4(), lane);
+        const f32x4 acc = mm16x3<KP>((kind ? s_kh : s_qh) + 16 * ti * LKH, (kind ? s_kl : s_ql) + 16 * ti * LKH,
+                                     LKH, s_s0h + 16 * tj * LKH, s_s0l + 16 * tj * LKH, LKH, zero4(), lane);
         const int col = 16 * tj + (lane & 15);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -213,6 +279,12 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
     }
   }
   __syncthreads();  // S0 region reused below
+  if constexpr (DK < KP) {
+    for (int i = tid; i < 2 * kBc * (KP - DK); i += kHT) {
+      const int r = i / (KP - DK), c = DK + i % (KP - DK);
+      s_kch[r * LKH + c] = 0;  // hi and lo planes are contiguous
+    }
+  }
 
   // ---- phase B: forward substitution over the blocks
   for (int jb = 0; jb < NBv; ++jb) {
@@ -256,18 +328,22 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
       for (int i = tid; i < kBc * (DK / 4); i += kHT) {
         const int r = i / (DK / 4), c4 = i % (DK / 4);
         const int pos = kBc * cb + r;
-        *reinterpret_cast<float4*>(s_kc + r * LK + 4 * c4) =
-            *reinterpret_cast<const float4*>(Fb + pos * C + nq + g * DK + 4 * c4);
+        st_split4(s_kch + r * LKH + 4 * c4, s_kcl + r * LKH + 4 * c4,
+                  *reinterpret_cast<const float4*>(Fb + pos * C + nq + g * DK + 4 * c4));
       }
-      for (int i = tid; i < kBc * (DV / 4); i += kHT) {
-        const int r = i / (DV / 4), c4 = i % (DV / 4);
-        *reinterpret_cast<float4*>(s_uc + r * LV + 4 * c4) =
-            *reinterpret_cast<const float4*>(Ub + size_t(kBc * cb + r) * DV + 4 * c4);
+      for (int i = tid; i < kBc * (DV / 4); i += kHT) {  // U_c transposed: [dv][node]
+        const int r = i % kBc, c4 = i / kBc;
+        const float4 u = *reinterpret_cast<const float4*>(Ub + size_t(kBc * cb + r) * DV + 4 * c4);
+        st_split1(s_uth + (4 * c4) * UL + r, s_utl + (4 * c4) * UL + r, u.x);
+        st_split1(s_uth + (4 * c4 + 1) * UL + r, s_utl + (4 * c4 + 1) * UL + r, u.y);
+        st_split1(s_uth + (4 * c4 + 2) * UL + r, s_utl + (4 * c4 + 2) * UL + r, u.z);
+        st_split1(s_uth + (4 * c4 + 3) * UL + r, s_utl + (4 * c4 + 3) * UL + r, u.w);
       }
       __syncthreads();
       {  // -X_jc (waves 0-3) and Y_jc (waves 4-7), one 16 x 16 tile each
         const int kind = wave >> 2, ti = (wave >> 1) & 1, tc = wave & 1;
-        const f32x4 acc = mm16<DK, true>((kind ? s_q : s_k) + 16 * ti * LK, LK, s_kc + 16 * tc * LK, LK, zero4(), lane);
+        const f32x4 acc = mm16x3<KP>((kind ? s_qh : s_kh) + 16 * ti * LKH, (kind ? s_ql : s_kl) + 16 * ti * LKH,
+                                     LKH, s_kch + 16 * tc * LKH, s_kcl + 16 * tc * LKH, LKH, zero4(), lane);
         const int c = 16 * tc + (lane & 15), pc = kBc * cb + c;
         const int nd = s_ord[pc];
 #pragma unroll
@@ -277,9 +353,9 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
           if (pi < nval && pc < nval && ((s_anc[i * kHW + (nd >> 6)] >> (nd & 63)) & 1ull))
             val = expf(s_la[pi] - s_la[pc]) * acc[r];
           if (kind == 0)
-            s_x[i * kLs + c] = -(pi < nval ? s_be[pi] : 0.0f) * val;
+            st_split1(s_xh + i * UL + c, s_xl + i * UL + c, -(pi < nval ? s_be[pi] : 0.0f) * val);
           else
-            s_y[i * kLs + c] = val;
+            st_split1(s_yh + i * UL + c, s_yl + i * UL + c, val);
         }
       }
       __syncthreads();
@@ -288,8 +364,10 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
         const int t = wave + 8 * u;
         if (t < NTILE) {
           const int ti = t / NTV, tj = t % NTV;
-          rr[u] = mm16<kBc, false>(s_x + 16 * ti * kLs, kLs, s_uc + 16 * tj, LV, rr[u], lane);
-          oo[u] = mm16<kBc, false>(s_y + 16 * ti * kLs, kLs, s_uc + 16 * tj, LV, oo[u], lane);
+          rr[u] = mm16x3<kBc>(s_xh + 16 * ti * UL, s_xl + 16 * ti * UL, UL, s_uth + 16 * tj * UL,
+                              s_utl + 16 * tj * UL, UL, rr[u], lane);
+          oo[u] = mm16x3<kBc>(s_yh + 16 * ti * UL, s_yl + 16 * ti * UL, UL, s_uth + 16 * tj * UL,
+                              s_utl + 16 * tj * UL, UL, oo[u], lane);
         }
       }
       __syncthreads();
@@ -297,7 +375,8 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
     // ---- diagonal block: A = -X_jj, M0 = I + A, Y_jj; R_j -> LDS
     {
       const int kind = wave >> 2, ti = (wave >> 1) & 1, tc = wave & 1;
-      const f32x4 acc = mm16<DK, true>((kind ? s_q : s_k) + 16 * ti * LK, LK, s_k + 16 * tc * LK, LK, zero4(), lane);
+      const f32x4 acc = mm16x3<KP>((kind ? s_qh : s_kh) + 16 * ti * LKH, (kind ? s_ql : s_kl) + 16 * ti * LKH,
+                                   LKH, s_kh + 16 * tc * LKH, s_kl + 16 * tc * LKH, LKH, zero4(), lane);
       const int c = 16 * tc + (lane & 15), pc = kBc * jb + c;
       const int nd = s_ord[pc];
 #pragma unroll
@@ -358,7 +437,7 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = 16 * ti + 4 * (lane >> 4) + r, pos = kBc * jb + row;
-          s_uc[row * LV + col] = d[r];
+          s_uj[row * LV + col] = d[r];
           if (pos < T) Ub[size_t(pos) * DV + col] = d[r];
         }
       }
@@ -370,7 +449,7 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
       const int t = wave + 8 * u;
       if (t < NTILE) {
         const int ti = t / NTV, tj = t % NTV, col = 16 * tj + (lane & 15);
-        const f32x4 d = mm16<kBc, false>(s_y + 16 * ti * kLs, kLs, s_uc + 16 * tj, LV, oo[u], lane);
+        const f32x4 d = mm16<kBc, false>(s_y + 16 * ti * kLs, kLs, s_uj + 16 * tj, LV, oo[u], lane);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pos = kBc * jb + 16 * ti + 4 * (lane >> 4) + r;
