@@ -148,7 +148,10 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   constexpr int KP = SM::KP, LKH = SM::LKH, LV = SM::LV, UL = SM::UL;
   constexpr int NTV = DV / 16;    // tiles across dv
   constexpr int NTILE = 2 * NTV;  // tiles of a 32 x DV block matrix
+  constexpr int NKP = (kBc * DK / 4 + kHT - 1) / kHT;  // float4 of a block's keys per thread
+  constexpr int NUP = (kBc * DV / 4 + kHT - 1) / kHT;  // float4 of a block's U rows per thread
   extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ uint32_t s_need;  // earlier blocks holding ancestors of the current block's nodes
   uint16_t* s_qh = reinterpret_cast<uint16_t*>(smem);  // block q~ planes [32][LKH]
   uint16_t* s_ql = s_qh + kBc * LKH;
   uint16_t* s_kh = s_ql + kBc * LKH;                    // block k~ planes
@@ -313,32 +316,64 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
       }
     }
     __syncthreads();
-    for (int cb = 0; cb < jb; ++cb) {
-      // does block cb hold an ancestor of a node of block jb?
-      int any = 0;
-      for (int pr = tid; pr < kBc * kBc; pr += kHT) {
-        const int i = pr & 31, c = pr >> 5;
-        const int pc = kBc * cb + c;
+    // the earlier blocks that hold an ancestor of a node of this block (one
+    // bit per block); their keys and U rows are loaded one block ahead
+    if (tid == 0) s_need = 0u;
+    __syncthreads();
+    {
+      uint32_t mask = 0u;
+      for (int pr = tid; pr < kBc * kBc * jb; pr += kHT) {
+        const int i = pr % kBc, pc = pr / kBc;
         if (kBc * jb + i < nval && pc < nval) {
           const int nd = s_ord[pc];
-          any |= int((s_anc[i * kHW + (nd >> 6)] >> (nd & 63)) & 1ull);
+          if ((s_anc[i * kHW + (nd >> 6)] >> (nd & 63)) & 1ull) mask |= 1u << (pc / kBc);
         }
       }
-      if (!__syncthreads_or(any)) continue;
-      for (int i = tid; i < kBc * (DK / 4); i += kHT) {
-        const int r = i / (DK / 4), c4 = i % (DK / 4);
-        const int pos = kBc * cb + r;
-        st_split4(s_kch + r * LKH + 4 * c4, s_kcl + r * LKH + 4 * c4,
-                  *reinterpret_cast<const float4*>(Fb + pos * C + nq + g * DK + 4 * c4));
+      if (mask) atomicOr(&s_need, mask);
+    }
+    __syncthreads();
+    uint32_t need = s_need;
+    float4 kpf[NKP], upf[NUP];
+    auto fetch = [&](int cb) {
+#pragma unroll
+      for (int j = 0; j < NKP; ++j) {
+        const int i = j * kHT + tid;
+        const int r = i < kBc * (DK / 4) ? i / (DK / 4) : 0, c4 = i < kBc * (DK / 4) ? i % (DK / 4) : 0;
+        kpf[j] = *reinterpret_cast<const float4*>(Fb + (kBc * cb + r) * C + nq + g * DK + 4 * c4);
       }
-      for (int i = tid; i < kBc * (DV / 4); i += kHT) {  // U_c transposed: [dv][node]
-        const int r = i % kBc, c4 = i / kBc;
-        const float4 u = *reinterpret_cast<const float4*>(Ub + size_t(kBc * cb + r) * DV + 4 * c4);
-        st_split1(s_uth + (4 * c4) * UL + r, s_utl + (4 * c4) * UL + r, u.x);
-        st_split1(s_uth + (4 * c4 + 1) * UL + r, s_utl + (4 * c4 + 1) * UL + r, u.y);
-        st_split1(s_uth + (4 * c4 + 2) * UL + r, s_utl + (4 * c4 + 2) * UL + r, u.z);
-        st_split1(s_uth + (4 * c4 + 3) * UL + r, s_utl + (4 * c4 + 3) * UL + r, u.w);
+#pragma unroll
+      for (int j = 0; j < NUP; ++j) {
+        const int i = j * kHT + tid;
+        const int r = i < kBc * (DV / 4) ? i % kBc : 0, c4 = i < kBc * (DV / 4) ? i / kBc : 0;
+        upf[j] = *reinterpret_cast<const float4*>(Ub + size_t(kBc * cb + r) * DV + 4 * c4);
       }
+    };
+    int cb = need ? __ffs(int(need)) - 1 : -1;
+    if (cb >= 0) fetch(cb);
+    while (cb >= 0) {
+#pragma unroll
+      for (int j = 0; j < NKP; ++j) {
+        const int i = j * kHT + tid;
+        if (i < kBc * (DK / 4)) {
+          const int r = i / (DK / 4), c4 = i % (DK / 4);
+          st_split4(s_kch + r * LKH + 4 * c4, s_kcl + r * LKH + 4 * c4, kpf[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < NUP; ++j) {  // U_c transposed: [dv][node]
+        const int i = j * kHT + tid;
+        if (i < kBc * (DV / 4)) {
+          const int r = i % kBc, c4 = i / kBc;
+          const float4 u = upf[j];
+          st_split1(s_uth + (4 * c4) * UL + r, s_utl + (4 * c4) * UL + r, u.x);
+          st_split1(s_uth + (4 * c4 + 1) * UL + r, s_utl + (4 * c4 + 1) * UL + r, u.y);
+          st_split1(s_uth + (4 * c4 + 2) * UL + r, s_utl + (4 * c4 + 2) * UL + r, u.z);
+          st_split1(s_uth + (4 * c4 + 3) * UL + r, s_utl + (4 * c4 + 3) * UL + r, u.w);
+        }
+      }
+      need &= need - 1u;
+      const int nb = need ? __ffs(int(need)) - 1 : -1;
+      if (nb >= 0) fetch(nb);  // the next block's loads fly during this one
       __syncthreads();
       {  // -X_jc (waves 0-3) and Y_jc (waves 4-7), one 16 x 16 tile each
         const int kind = wave >> 2, ti = (wave >> 1) & 1, tc = wave & 1;
@@ -371,6 +406,7 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
         }
       }
       __syncthreads();
+      cb = nb;
     }
     // ---- diagonal block: A = -X_jj, M0 = I + A, Y_jj; R_j -> LDS
     {
