@@ -191,3 +191,28 @@ def test_large_step_path_lengths(G, orc):
     wp.accepted[:] = depths
     _announce(f"large-T step path lengths {[d + 1 for d in depths]}")
     _step_check(G, orc, wp, wc)
+
+
+def test_two_streams_share_nothing(G, orc):
+    """Trees above 128 slots on two streams at once, different sizes: each
+    stream gets its own cached workspace, so the results equal the oracle's
+    (and are the same as when run one after the other)."""
+    import torch
+    wa = W.make_random(7400, 2, 300, 1, 2, 64, 64, "bf16", shuffle=True)
+    wb = W.make_random(7401, 3, 180, 2, 4, 32, 32, "bf16", shuffle=True)
+    da, db = G.DeviceTree(wa), G.DeviceTree(wb)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    for s, d in ((sa, da), (sb, db)):
+        s.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):   # interleaved launches on the two streams
+        with torch.cuda.stream(sa):
+            da.prepare(stream=sa)
+            da.verify(stream=sa)
+        with torch.cuda.stream(sb):
+            db.prepare(stream=sb)
+            db.verify(stream=sb)
+    torch.cuda.synchronize()
+    for w, d in ((wa, da), (wb, db)):
+        ref = orc.verify(w)
+        got = d.out.cpu().numpy().astype(np.float64)
+        assert np.max(np.abs(got - ref)) <= O_TOL * np.max(np.abs(ref))

@@ -425,3 +425,39 @@ def test_custom_scale(orc):
     o1 = orc.verify(w)
     o2 = orc.verify(w, scale=0.5)
     np.testing.assert_allclose(o2, o1 * 0.5 * np.sqrt(w.dk), rtol=1e-13, atol=1e-15)
+
+
+def test_recurrence_exact_rationals(orc):
+    """Eq. 7-8 in exact rational arithmetic on 7-node trees (dk = 4, so the
+    readout scale 1/2 is exact, dv = 3): starting from the post-conv features
+    the oracle uses, every node's output and the committed state agree with
+    the exact values to rounding."""
+    from fractions import Fraction as Fr
+    for seed, par in ((71, [-1, 0, 0, 1, 1, 2, 2]), (72, [3, 3, -1, 2, 0, 4, 0])):
+        w = _small(seed, par, Hk=1, Hv=2, dk=4, dv=3)
+        feat = orc.features(w)
+        out = orc.verify(w)
+        S_new, _cs, _st = orc.commit(w)
+        nq = w.Hk * w.dk
+        al, be = _f64(w, "alpha"), _f64(w, "beta")
+
+        def walk(i, h):
+            S = [[Fr(float(x)) for x in row] for row in _f64(w, "S0")[0, h]]  # [dv][dk]
+            for t in _path(w.parent[0].tolist(), i):
+                k = [Fr(float(x)) for x in feat[0, t, nq: nq + w.dk]]
+                v = [Fr(float(x)) for x in feat[0, t, 2 * nq + h * w.dv: 2 * nq + (h + 1) * w.dv]]
+                a, b_ = Fr(float(al[0, t, h])), Fr(float(be[0, t, h]))
+                Sk = [sum(S[r][c] * k[c] for c in range(w.dk)) for r in range(w.dv)]
+                S = [[a * (S[r][c] - b_ * Sk[r] * k[c]) + b_ * v[r] * k[c] for c in range(w.dk)]
+                     for r in range(w.dv)]
+            return S
+
+        for h in range(w.Hv):
+            for i in range(w.T):
+                S = walk(i, h)
+                q = [Fr(float(x)) for x in feat[0, i, :w.dk]]
+                o = [Fr(1, 2) * sum(S[r][c] * q[c] for c in range(w.dk)) for r in range(w.dv)]
+                np.testing.assert_allclose(out[0, i, h], [float(x) for x in o], rtol=1e-13, atol=1e-15)
+            S = walk(int(w.accepted[0]), h)
+            np.testing.assert_allclose(S_new[0, h], [[float(x) for x in row] for row in S], rtol=1e-13,
+                                       atol=1e-15)

@@ -430,3 +430,38 @@ def test_wide_dynamic_range_step(G, orc):
     _announce(f"wide dynamic range step: per-channel out err {err:.3e}  per-row state err {serr:.3e}")
     assert err <= WIDE_TOL
     assert serr <= S_TOL
+
+
+@pytest.mark.parametrize("T", [60, 300])
+def test_nan_reaches_only_descendants(G, orc, T):
+    """Failure containment: a NaN in the raw value of node j (one value
+    head) reaches the outputs of j's descendants (and j) in that head only;
+    every other output is bit-identical to the clean run (on-chip kernel at
+    T = 60, workspace path at T = 300)."""
+    import torch
+    w = W.make_random(3800 + T, 2, T, 1, 2, 32, 32, "f32", shuffle=True)
+    ref = orc.prepare(w.parent)
+    b, j, h = 1, int(np.nonzero(w.parent[1] >= 0)[0][3]), 1
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    dt.verify()
+    torch.cuda.synchronize()
+    clean = dt.out.clone()
+    v = dt.v.clone()
+    v[b, j, h, 5] = float("nan")
+    dt.v = v
+    dt.verify()
+    torch.cuda.synchronize()
+    got = dt.out.cpu().numpy()
+    base = clean.cpu().numpy()
+    desc = np.zeros(T, bool)
+    for i in range(T):
+        anc = [(int(ref["anc"][b, i, t // 64]) >> (t % 64)) & 1 for t in range(T)]
+        desc[i] = i == j or anc[j] == 1
+    bad = ~np.isfinite(got).all(axis=-1)           # [B][T][Hv]
+    assert bad[b, j, h]
+    assert not bad[:, :, 1 - h].any() and not bad[1 - b].any()
+    assert not (bad[b, :, h] & ~desc).any()
+    keep = np.ones(got.shape[:3], bool)
+    keep[b, desc, h] = False
+    np.testing.assert_array_equal(got[keep].view(np.int32), base[keep].view(np.int32))
