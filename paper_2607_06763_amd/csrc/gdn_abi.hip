@@ -5,6 +5,10 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
+#include <set>
+#include <utility>
+
 #include "gdn_internal.h"
 
 namespace gdn {
@@ -17,6 +21,19 @@ int set_error(int code, const char* fmt, ...) {
   vsnprintf(g_err, sizeof(g_err), fmt, ap);
   va_end(ap);
   return code;
+}
+
+int ensure_dynamic_lds(const void* fn, int bytes, const char* who) {
+  static std::mutex mu;
+  static std::set<std::pair<const void*, int>> done;  // (kernel, device)
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return set_error(GDN_EHIP, "%s: hipGetDevice failed", who);
+  std::lock_guard<std::mutex> lock(mu);
+  if (done.count({fn, dev})) return GDN_OK;
+  const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return set_error(GDN_EHIP, "%s: LDS attribute: %s", who, hipGetErrorString(e));
+  done.insert({fn, dev});
+  return GDN_OK;
 }
 
 static bool head_dim_ok(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }

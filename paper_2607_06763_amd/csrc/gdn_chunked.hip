@@ -503,13 +503,9 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
 template <int DK, int DV, typename TIn>
 static int launch_chunk_t(const ChunkParams& p, hipStream_t stream) {
   using SM = ChunkSmem<DK, DV>;
-  static bool attr = false;  // the maximum dynamic LDS is set once per process
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&chunk_kernel<DK, DV, TIn>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(SM::total));
-    if (e != hipSuccess) return set_error(GDN_EHIP, "verify_chunked: LDS attribute: %s", hipGetErrorString(e));
-    attr = true;
-  }
+  const int rc = ensure_dynamic_lds(reinterpret_cast<const void*>(&chunk_kernel<DK, DV, TIn>), int(SM::total),
+                                    "verify_chunked");
+  if (rc != GDN_OK) return rc;
   hipLaunchKernelGGL((chunk_kernel<DK, DV, TIn>), dim3(p.Hv, p.B), dim3(kHT), SM::total, stream, p);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify_chunked launch: %s", hipGetErrorString(e));

@@ -378,4 +378,8 @@ int launch_commit(const CommitArgs& a, hipStream_t stream);
 // Records a message for gdn_last_error() and returns code.
 int set_error(int code, const char* fmt, ...);
 
+// Raises the dynamic-LDS limit of kernel fn to bytes on the current device,
+// once per (kernel, device); thread-safe.  Returns a gdn_status.
+int ensure_dynamic_lds(const void* fn, int bytes, const char* who);
+
 }  // namespace gdn

@@ -345,13 +345,9 @@ static int launch_large_t(const LargeParams& p, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
   using SM = PullSmem<DK, DV>;
-  static bool attr = false;  // the maximum dynamic LDS is set once per process
-  if (!attr) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&pull_kernel<DK, DV, TIn>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, int(SM::total));
-    if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) LDS attribute: %s", hipGetErrorString(e));
-    attr = true;
-  }
+  const int rc = ensure_dynamic_lds(reinterpret_cast<const void*>(&pull_kernel<DK, DV, TIn>), int(SM::total),
+                                    "verify (T > 128)");
+  if (rc != GDN_OK) return rc;
   hipLaunchKernelGGL((pull_kernel<DK, DV, TIn>), dim3(p.Hv, p.B), dim3(kLT), SM::total, stream, p);
   e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) launch: %s", hipGetErrorString(e));

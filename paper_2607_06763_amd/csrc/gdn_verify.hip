@@ -1248,15 +1248,9 @@ static int launch_verify_t(const VerifyArgs& a, int hpw, int ns, hipStream_t str
   p.S = a.S;
   p.commit_status = a.commit_status;
   const size_t smem = verify_smem(a.T, DK, DVS, FUSED).total;
-  static bool attr_done = false;
-  if (!attr_done) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&verify_kernel<DK, DVS, TIn, FUSED>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(verify_smem(kVMaxT, DK, DVS, FUSED).total));
-    if (e != hipSuccess)
-      return set_error(GDN_EHIP, "verify: LDS attribute: %s", hipGetErrorString(e));
-    attr_done = true;
-  }
+  const int rc = ensure_dynamic_lds(reinterpret_cast<const void*>(&verify_kernel<DK, DVS, TIn, FUSED>),
+                                    int(verify_smem(kVMaxT, DK, DVS, FUSED).total), "verify");
+  if (rc != GDN_OK) return rc;
   const int G = a.Hv / a.Hk;
   hipLaunchKernelGGL((verify_kernel<DK, DVS, TIn, FUSED>), dim3(ns, a.Hk * (G / hpw), a.B), dim3(kVT), smem,
                      stream, p);
