@@ -129,8 +129,10 @@ int gdn_tree_prepare(const gdn_dims* dims, const int32_t* parent, void* meta,
 
 /* Read-only tree verification (Sec. 3.4: Eq. 7-8 per node along its path).
  * Up to 128 slots everything stays on chip and nothing is allocated; above
- * 128 the post-conv features go through a device workspace of B T C 4 bytes
- * that the library allocates on the first call that needs it and keeps per
+ * 128 the post-conv features go through a device workspace of
+ * B T (2 C + 4 Hv) bytes (fp16 features, fp32 scales of the value rows;
+ * C = 2 Hk dk + Hv dv, the first part rounded up to 256 bytes) that the
+ * library allocates on the first call that needs it and keeps per
  * (device, stream) until the process ends (a call under stream capture that
  * would have to grow it returns GDN_EUNSUPPORTED).
  *   meta        written by gdn_tree_prepare for the same B, T
@@ -151,7 +153,7 @@ int gdn_tree_verify(const gdn_dims* dims, const void* meta, const void* q, const
  * under HIP graph capture, serving loops that forbid hipMalloc).  Same
  * arguments, layouts, outputs and errors as gdn_tree_verify, whose kernels
  * it runs; it calls no allocating routine.  Trees of more than 128 slots
- * need a feature workspace of B * T * C * 4 bytes (C = 2 Hk dk + Hv dv):
+ * need the feature workspace of gdn_tree_verify, B T (2 C + 4 Hv) bytes:
  * here it is a static device array of GDN_NOALLOC_SCRATCH_BYTES that the
  * library holds on every device it runs on until the process ends, and
  * larger problems return GDN_EUNSUPPORTED before any device work.  All
@@ -170,7 +172,9 @@ int gdn_tree_verify_noalloc(const gdn_dims* dims, const void* meta, const void* 
  * self: decayed query-key products) are built from Gram products, (I + X) U =
  * beta (V - a K S0^T) is solved by forward substitution over sub-blocks of 32
  * positions (each diagonal block inverted by repeated squaring), and O =
- * scale (a Q S0^T + Y U); every dense product on fp32 MFMA.  Arguments,
+ * scale (a Q S0^T + Y U); the Gram, solve and readout products on bf16
+ * MFMA as hi/lo three-product splits (about 16 significant bits), the
+ * diagonal-block inverses on fp32 MFMA, features in fp32.  Arguments,
  * layouts, outputs and errors are those of gdn_tree_verify (any supported
  * dk, dv and T).  Needs a workspace of B T (C + Hv dv) 4 bytes, cached per
  * (device, stream) like gdn_tree_verify's above 128 slots.  Its cost does not

@@ -65,7 +65,7 @@ static int verify_any(const VerifyArgs& a, hipStream_t stream) {
   int rc = GDN_OK;
   void* ws = stream_workspace(bytes, stream, &rc);
   if (!ws) return rc;
-  return launch_verify_large(a, static_cast<float*>(ws), bytes, stream);
+  return launch_verify_large(a, ws, bytes, stream);
 }
 
 }  // namespace gdn

@@ -77,7 +77,7 @@ struct ChunkSmem {
 };
 
 size_t chunked_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
-  return large_workspace_bytes(B, T, Hk, Hv, dk, dv) + size_t(B) * Hv * size_t(T) * dv * sizeof(float);
+  return features_f32_bytes(B, T, Hk, Hv, dk, dv) + size_t(B) * Hv * size_t(T) * dv * sizeof(float);
 }
 
 // acc += A (16 x K) B (K x 16) for one 16 x 16 tile on v_mfma_f32_16x16x4f32.
@@ -553,7 +553,7 @@ int launch_verify_chunked(const VerifyArgs& a, void* ws, size_t ws_bytes, hipStr
   p.S0 = a.S0;
   p.out = a.out;
   p.F = F;
-  p.U = F + large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv) / sizeof(float);
+  p.U = F + features_f32_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv) / sizeof(float);
   if (a.in_dtype == GDN_BF16) return chunk_dk<BF16>(a.dk, a.dv, p, stream);
   return chunk_dk<float>(a.dk, a.dv, p, stream);
 }

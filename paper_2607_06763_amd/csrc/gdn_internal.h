@@ -344,10 +344,10 @@ struct VerifyArgs {
   int32_t* commit_status = nullptr;
 };
 int launch_verify(const VerifyArgs& a, hipStream_t stream);
-// trees of 129..512 slots: features into the workspace, then the pull-back
-// (the workspace holds large_workspace_bytes(...) bytes)
+// trees of 129..512 slots: fp16 features into the workspace, then the
+// pull-back (the workspace holds large_workspace_bytes(...) bytes)
 size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv);
-int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStream_t stream);
+int launch_verify_large(const VerifyArgs& a, void* ws, size_t ws_bytes, hipStream_t stream);
 // A device buffer of at least bytes for work on stream, cached per (device,
 // stream) and grown on demand (never while the stream is being captured).
 void* stream_workspace(size_t bytes, hipStream_t stream, int* rc);
@@ -355,7 +355,9 @@ void* stream_workspace(size_t bytes, hipStream_t stream, int* rc);
 // library's static device array
 int launch_verify_noalloc(const VerifyArgs& a, hipStream_t stream);
 // post-conv features of every position into F[B][T][C] (fp32, canonical
-// position order; large_workspace_bytes(...) bytes)
+// position order; features_f32_bytes(...) bytes), as the chunked form reads
+// them
+size_t features_f32_bytes(int B, int T, int Hk, int Hv, int dk, int dv);
 int launch_features(const VerifyArgs& a, float* F, hipStream_t stream);
 // the paper's chunked form (Eq. 9-13) of the same verification; ws holds
 // chunked_workspace_bytes(...) bytes

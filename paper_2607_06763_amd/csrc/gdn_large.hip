@@ -11,14 +11,22 @@
 //   feat_kernel   one workgroup per (1024 channels, 32 positions, sequence):
 //                 the width-4 conv along each node's path (conv-state slots
 //                 above the root), SiLU, and the per-head L2 norm of q and
-//                 k; written to a workspace F[B][T][C] (fp32, canonical
-//                 position order, channels as in conv_w)
+//                 k; written to a workspace of fp16 features FH[B][T][C]
+//                 (canonical position order, channels as in conv_w; q~
+//                 and k~ have unit norm, each v~ row of a value head is
+//                 scaled by the power of two that puts its largest
+//                 magnitude in [1, 2), the inverse scale kept in
+//                 Vs[B][T][Hv]).  The chunked form reads the same features
+//                 as fp32 (launch_features).
 //   pull_kernel   one workgroup per (value head, sequence), 512 threads:
 //                 the head's S0 as one fp16 plane in LDS (each row scaled by
 //                 the power of two that puts its largest magnitude in [1, 2),
 //                 exact, undone on the output), then tiles of 32 positions:
 //                 16 lanes per node walk the paths with the features of the
-//                 path nodes gathered from F (two steps of loads ahead),
+//                 path nodes gathered from FH (two steps of loads ahead;
+//                 fp16 operands into fp32 accumulators by mixed-precision
+//                 FMAs), the value heads of one key head on one XCD so that
+//                 they share its k~ rows in L2,
 //                 r x -> an fp16 tile, O^T = S0 (r X)^T on
 //                 v_mfma_f32_16x16x32_f16 (fp32 accumulation), plus acc.
 #include <map>
@@ -40,10 +48,20 @@ struct LargeParams {
   const void *q, *k, *v, *alpha, *beta;
   const float *conv_w, *conv_state, *S0;
   float* out;
-  float* F;  // workspace [B][T][C]
+  float* F;       // fp32 features [B][T][C] (chunked form)
+  _Float16* FH;   // fp16 features [B][T][C] (pull-back)
+  float* Vs;      // inverse v~ row scales [B][T][Hv] (pull-back)
 };
 
+static size_t fh_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
+  return (size_t(B) * size_t(T) * size_t(2 * Hk * dk + Hv * dv) * 2 + 255) & ~size_t(255);
+}
+
 size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
+  return fh_bytes(B, T, Hk, Hv, dk, dv) + size_t(B) * size_t(T) * size_t(Hv) * sizeof(float);
+}
+
+size_t features_f32_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
   return size_t(B) * size_t(T) * size_t(2 * Hk * dk + Hv * dv) * sizeof(float);
 }
 
@@ -57,8 +75,19 @@ size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
 constexpr int kFP = 32;  // positions per feature workgroup
 constexpr int kFU = 4;   // positions whose loads are in flight together
 
-template <typename TIn, int DK>
+// First thread (in units of 4 channels) of the value channels.  For the
+// fp16 features the value heads start on a 32-lane boundary, so that the
+// DV / 4 lanes of each head are aligned consecutive lanes (one row max).
+__host__ __device__ inline int feat_vbase4(int Hk, int dk, bool half) {
+  const int nqk4 = 2 * Hk * dk / 4;
+  return half ? (nqk4 + 31) & ~31 : nqk4;
+}
+
+// VG = 0: fp32 features into p.F; VG = DV / 4: fp16 features into p.FH
+// with the v~ rows of each head scaled (inverse scales into p.Vs).
+template <typename TIn, int DK, int VG>
 __global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
+  constexpr bool kHalf = VG > 0;
   __shared__ int s_tap[kFP][4];  // node of each tap, or -1 - conv-state slot
   const int b = blockIdx.z, tid = threadIdx.x;
   const int p0 = blockIdx.y * kFP;
@@ -82,9 +111,11 @@ __global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
   }
   const int nq = Hk * DK;
   const int C = 2 * nq + Hv * DV;
+  const int vb4 = feat_vbase4(Hk, DK, kHalf);
   const int c4 = blockIdx.x * kFT + tid;
-  const bool ok = c4 < C / 4;
-  const int c = ok ? 4 * c4 : 0;
+  const bool isv = c4 >= vb4;
+  const bool ok = isv ? c4 - vb4 < Hv * DV / 4 : c4 < 2 * nq / 4;
+  const int c = ok ? (isv ? 2 * nq + 4 * (c4 - vb4) : 4 * c4) : 0;
   // this thread's channels: source tensor, row stride and offset
   const TIn* src;
   size_t stride;
@@ -101,32 +132,63 @@ __global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
   const float4* wr = reinterpret_cast<const float4*>(p.conv_w + size_t(c) * 4);
   const float4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
   const bool qk = c < 2 * nq;
-  float* dst = p.F + (bt + p0) * size_t(C) + c;
+  float* dst = kHalf ? nullptr : p.F + (bt + p0) * size_t(C) + c;
+  _Float16* dsth = kHalf ? p.FH + (bt + p0) * size_t(C) + c : nullptr;
+  // the first lane of each value head writes the head's inverse scale
+  const bool vs_lane = kHalf && ok && isv && (c4 - vb4) % (kHalf ? VG : 1) == 0;
+  float* vs = vs_lane ? p.Vs + (bt + p0) * size_t(Hv) + (c4 - vb4) / (kHalf ? VG : 1) : nullptr;
   __syncthreads();
+  // the three conv-state slots of this thread's channels (the same for every
+  // position): loaded once, so that every tap below is one unconditional
+  // row load and a select (a load under a branch waits for itself)
+  const float4 cs0 = ld4(cs), cs1 = ld4(cs + C), cs2 = ld4(cs + 2 * size_t(C));
+  // tap value: the loaded row, or for a tap above the root (code -1 - slot)
+  // the conv-state slot
+  auto pick = [&](const float4& raw, int code) {
+    const float4 c = code == -1 ? cs0 : (code == -2 ? cs1 : cs2);
+    return code >= 0 ? raw : c;
+  };
   for (int i0 = 0; i0 < np; i0 += kFU) {
-    float4 x[kFU][4];
+    float4 xr[kFU][4];
+    int code[kFU][3];
 #pragma unroll
     for (int u = 0; u < kFU; ++u) {
       const int i = i0 + u < np ? i0 + u : np - 1;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const int nd = s_tap[i][w];
-        x[u][w] = nd >= 0 ? ld4(src + size_t(nd) * stride) : ld4(cs + size_t(-1 - nd) * C);
+        if (w < 3) code[u][w] = nd;
+        xr[u][w] = ld4(src + size_t(nd >= 0 ? nd : 0) * stride);
       }
     }
 #pragma unroll
     for (int u = 0; u < kFU; ++u) {
+      const float4 x[4] = {pick(xr[u][0], code[u][0]), pick(xr[u][1], code[u][1]), pick(xr[u][2], code[u][2]),
+                           xr[u][3]};  // tap 3 is the node itself
       float y[4];
-      y[0] = silu(fmaf(w0.w, x[u][3].x, fmaf(w0.z, x[u][2].x, fmaf(w0.y, x[u][1].x, w0.x * x[u][0].x))));
-      y[1] = silu(fmaf(w1.w, x[u][3].y, fmaf(w1.z, x[u][2].y, fmaf(w1.y, x[u][1].y, w1.x * x[u][0].y))));
-      y[2] = silu(fmaf(w2.w, x[u][3].z, fmaf(w2.z, x[u][2].z, fmaf(w2.y, x[u][1].z, w2.x * x[u][0].z))));
-      y[3] = silu(fmaf(w3.w, x[u][3].w, fmaf(w3.z, x[u][2].w, fmaf(w3.y, x[u][1].w, w3.x * x[u][0].w))));
+      y[0] = silu(fmaf(w0.w, x[3].x, fmaf(w0.z, x[2].x, fmaf(w0.y, x[1].x, w0.x * x[0].x))));
+      y[1] = silu(fmaf(w1.w, x[3].y, fmaf(w1.z, x[2].y, fmaf(w1.y, x[1].y, w1.x * x[0].y))));
+      y[2] = silu(fmaf(w2.w, x[3].z, fmaf(w2.z, x[2].z, fmaf(w2.y, x[1].z, w2.x * x[0].z))));
+      y[3] = silu(fmaf(w3.w, x[3].w, fmaf(w3.z, x[2].w, fmaf(w3.y, x[1].w, w3.x * x[0].w))));
       // the DK / 4 lanes of a q or k head are consecutive lanes of one wave
       float ss = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
       ss = group_sum<DK / 4>(ss);
       const float f = qk ? rsqrt_hw(ss + 1e-6f) : 1.0f;
-      if (ok && i0 + u < np)
-        *reinterpret_cast<float4*>(dst + size_t(i0 + u) * C) = make_float4(y[0] * f, y[1] * f, y[2] * f, y[3] * f);
+      if constexpr (kHalf) {
+        // v~: one power-of-two scale per (position, head) from the row max
+        float mx = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
+        mx = group_max<VG>(mx);
+        float sc, inv;
+        row_scale(mx, sc, inv);
+        if (ok && i0 + u < np) {
+          *reinterpret_cast<uint2*>(dsth + size_t(i0 + u) * C) =
+              to_f16x4(make_float4(y[0], y[1], y[2], y[3]), qk ? f : sc);
+          if (vs_lane) vs[size_t(i0 + u) * Hv] = inv;
+        }
+      } else {
+        if (ok && i0 + u < np)
+          *reinterpret_cast<float4*>(dst + size_t(i0 + u) * C) = make_float4(y[0] * f, y[1] * f, y[2] * f, y[3] * f);
+      }
     }
   }
 }
@@ -142,7 +204,7 @@ struct PullSmem {
   static constexpr size_t xt = size_t(kLTile) * KP * 2;
   static constexpr size_t pt = size_t(kLTile) * PP * 4;
   static constexpr size_t inv = size_t(DV) * 4;
-  static constexpr size_t meta = size_t(kLMaxT) * (2 + 2 + 4 + 4);
+  static constexpr size_t meta = size_t(kLMaxT) * (2 + 2 + 4 + 4 + 4);
   static constexpr size_t total = plane + xt + pt + inv + meta;
 };
 
@@ -163,6 +225,18 @@ __device__ __forceinline__ void ld_f(const float* src, float (&x)[N]) {
   }
 }
 
+// N consecutive fp16 values (N = 1, 2, 4, 8, aligned to 2 N bytes) as one
+// load, kept packed in registers.
+template <int N>
+struct HalfVec {
+  typedef _Float16 type __attribute__((ext_vector_type(N)));
+};
+template <int N>
+__device__ __forceinline__ typename HalfVec<N>::type ld_h(const _Float16* src) {
+  static_assert(N == 1 || N == 2 || N == 4 || N == 8, "fp16 vector width");
+  return *reinterpret_cast<const typename HalfVec<N>::type*>(src);
+}
+
 template <int DK, int DV, typename TIn>
 __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   using SM = PullSmem<DK, DV>;
@@ -178,11 +252,19 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   int16_t* s_ppos = s_ord + kLMaxT;
   float* s_al = reinterpret_cast<float*>(s_ppos + kLMaxT);
   float* s_be = s_al + kLMaxT;
+  float* s_vs = s_be + kLMaxT;  // inverse v~ row scales by position
 
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  // Blocks go round-robin over the 8 XCDs: the G value heads of unit u =
+  // (sequence, key head), which gather the same k~ rows, take blocks
+  // u % 8 + 8 j of their group of 8 G, i.e. one XCD and one L2.
   const int T = p.T, Hk = p.Hk, Hv = p.Hv;
-  const int g = h * Hk / Hv;
+  const int G = Hv / Hk;
+  const int grp = blockIdx.x / (8 * G), rem = blockIdx.x % (8 * G);
+  const int unit = 8 * grp + rem % 8;
+  if (unit >= p.B * Hk) return;  // uniform
+  const int b = unit / Hk, g = unit % Hk, h = g * G + rem / 8;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const int nq = Hk * DK;
   const size_t C = size_t(2 * nq + Hv * DV);
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
@@ -198,6 +280,7 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
     s_ppos[j] = int16_t(j < nval ? m.ppos[bt + j] : -1);
     s_al[j] = j < nval ? ld(alpha, (bt + nd) * Hv + h) : 0.0f;
     s_be[j] = j < nval ? ld(beta, (bt + nd) * Hv + h) : 0.0f;
+    s_vs[j] = j < nval ? p.Vs[(bt + j) * Hv + h] : 0.0f;
   }
   // ---- S0 -> fp16 plane (16 lanes per row), zero columns past DK
   if (nval > 0) {
@@ -231,7 +314,9 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   const float scale = p.scale;
   const int jn = wave * 4 + (lane >> 4);  // node slot of this lane in a tile
   const int ln = lane & 15;
-  const float* Fb = p.F + bt * C;
+  const _Float16* Fb = p.FH + bt * C;
+  using HK = typename HalfVec<CK>::type;
+  using HVv = typename HalfVec<CV>::type;
   for (int n0 = 0; n0 < T; n0 += kLTile) {
     const int pos = n0 + jn;
     const bool real = pos < nval;
@@ -242,52 +327,44 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 #pragma unroll
     for (int e = 0; e < CK; ++e) x[e] = 0.0f;
     if (real) {
-      ld_f<CK>(Fb + size_t(pos) * C + g * DK + ln * CK, x);
+      {
+        const HK q0 = ld_h<CK>(Fb + size_t(pos) * C + g * DK + ln * CK);
+#pragma unroll
+        for (int e = 0; e < CK; ++e) x[e] = (float)q0[e];
+      }
       // walk to the root; the path nodes' features load two steps ahead
-      const float* Fk = Fb + nq + g * DK + ln * CK;
-      const float* Fv = Fb + 2 * nq + h * DV + ln * CV;
+      const _Float16* Fk = Fb + nq + g * DK + ln * CK;
+      const _Float16* Fv = Fb + 2 * nq + h * DV + ln * CV;
       int t = pos;
       int t1 = s_ppos[t];
       int t2 = t1 >= 0 ? s_ppos[t1] : -1;
-      float kc[CK], vc[CV], k1[CK], v1[CV];
-      ld_f<CK>(Fk + size_t(t) * C, kc);
-      ld_f<CV>(Fv + size_t(t) * C, vc);
-      {
-        const size_t o1 = size_t(t1 >= 0 ? t1 : t) * C;  // clamped: not used past the root
-        ld_f<CK>(Fk + o1, k1);
-        ld_f<CV>(Fv + o1, v1);
-      }
+      HK kc = ld_h<CK>(Fk + size_t(t) * C);
+      HVv vc = ld_h<CV>(Fv + size_t(t) * C);
+      const size_t o1 = size_t(t1 >= 0 ? t1 : t) * C;  // clamped: not used past the root
+      HK k1 = ld_h<CK>(Fk + o1);
+      HVv v1 = ld_h<CV>(Fv + o1);
       while (t >= 0) {  // uniform per 16-lane node group
-        float k2[CK], v2[CV];
-        {
-          const size_t o2 = size_t(t2 >= 0 ? t2 : t) * C;
-          ld_f<CK>(Fk + o2, k2);
-          ld_f<CV>(Fv + o2, v2);
-        }
+        const size_t o2 = size_t(t2 >= 0 ? t2 : t) * C;
+        const HK k2 = ld_h<CK>(Fk + o2);
+        const HVv v2 = ld_h<CV>(Fv + o2);
         float s = 0.0f;
 #pragma unroll
-        for (int e = 0; e < CK; ++e) s = fmaf(kc[e], x[e], s);
+        for (int e = 0; e < CK; ++e) s = fmaf((float)kc[e], x[e], s);
         s = group_sum<16>(s);
         const float c = s_be[t] * s;
-        const float rc = r * c;
+        const float rc = r * c * s_vs[t];
 #pragma unroll
-        for (int e = 0; e < CV; ++e) acc[e] = fmaf(rc, vc[e], acc[e]);
+        for (int e = 0; e < CV; ++e) acc[e] = fmaf(rc, (float)vc[e], acc[e]);
 #pragma unroll
-        for (int e = 0; e < CK; ++e) x[e] = fmaf(-c, kc[e], x[e]);
+        for (int e = 0; e < CK; ++e) x[e] = fmaf(-c, (float)kc[e], x[e]);
         r *= s_al[t];
         t = t1;
         t1 = t2;
         t2 = t2 >= 0 ? s_ppos[t2] : -1;
-#pragma unroll
-        for (int e = 0; e < CK; ++e) {
-          kc[e] = k1[e];
-          k1[e] = k2[e];
-        }
-#pragma unroll
-        for (int e = 0; e < CV; ++e) {
-          vc[e] = v1[e];
-          v1[e] = v2[e];
-        }
+        kc = k1;
+        k1 = k2;
+        vc = v1;
+        v1 = v2;
       }
     }
     // r x -> fp16 tile row jn (zero for padding positions)
@@ -334,21 +411,22 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 // ---------------------------------------------------------------------------
 // Launch
 // ---------------------------------------------------------------------------
-static dim3 feat_grid(const LargeParams& p, int dk, int dv) {
-  const int n4 = (2 * p.Hk * dk + p.Hv * dv) / 4;
+static dim3 feat_grid(const LargeParams& p, int dk, int dv, bool half) {
+  const int n4 = feat_vbase4(p.Hk, dk, half) + p.Hv * dv / 4;
   return dim3((n4 + kFT - 1) / kFT, (p.T + kFP - 1) / kFP, p.B);
 }
 
 template <int DK, int DV, typename TIn>
 static int launch_large_t(const LargeParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((feat_kernel<TIn, DK>), feat_grid(p, DK, DV), dim3(kFT), 0, stream, p, DV);
+  hipLaunchKernelGGL((feat_kernel<TIn, DK, DV / 4>), feat_grid(p, DK, DV, true), dim3(kFT), 0, stream, p, DV);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
   using SM = PullSmem<DK, DV>;
   const int rc = ensure_dynamic_lds(reinterpret_cast<const void*>(&pull_kernel<DK, DV, TIn>), int(SM::total),
                                     "verify (T > 128)");
   if (rc != GDN_OK) return rc;
-  hipLaunchKernelGGL((pull_kernel<DK, DV, TIn>), dim3(p.Hv, p.B), dim3(kLT), SM::total, stream, p);
+  const int units = p.B * p.Hk, G = p.Hv / p.Hk;
+  hipLaunchKernelGGL((pull_kernel<DK, DV, TIn>), dim3((units + 7) / 8 * 8 * G), dim3(kLT), SM::total, stream, p);
   e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) launch: %s", hipGetErrorString(e));
   return GDN_OK;
@@ -376,7 +454,9 @@ static int large_dk(const VerifyArgs& a, const LargeParams& p, hipStream_t s) {
   return set_error(GDN_EUNSUPPORTED, "verify: dk=%d unsupported", a.dk);
 }
 
-static LargeParams large_params(const VerifyArgs& a, float* ws) {
+// ws: the pull-back workspace (fp16 features, then the v~ scales) or, for
+// launch_features, the fp32 feature array
+static LargeParams large_params(const VerifyArgs& a, void* ws, bool half) {
   LargeParams p;
   p.B = a.B;
   p.T = a.T;
@@ -393,15 +473,18 @@ static LargeParams large_params(const VerifyArgs& a, float* ws) {
   p.conv_state = a.conv_state;
   p.S0 = a.S0;
   p.out = a.out;
-  p.F = ws;
+  p.F = half ? nullptr : static_cast<float*>(ws);
+  p.FH = half ? static_cast<_Float16*>(ws) : nullptr;
+  p.Vs = half ? reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + fh_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv))
+              : nullptr;
   return p;
 }
 
-int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStream_t stream) {
+int launch_verify_large(const VerifyArgs& a, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (a.T > kLMaxT) return set_error(GDN_EUNSUPPORTED, "verify: T=%d exceeds %d", a.T, kLMaxT);
   if (ws_bytes < large_workspace_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv))
     return set_error(GDN_EINVAL, "verify: workspace of %zu bytes is too small", ws_bytes);
-  const LargeParams p = large_params(a, ws);
+  const LargeParams p = large_params(a, ws, true);
   if (a.in_dtype == GDN_BF16) return large_dk<BF16>(a, p, stream);
   return large_dk<float>(a, p, stream);
 }
@@ -409,10 +492,10 @@ int launch_verify_large(const VerifyArgs& a, float* ws, size_t ws_bytes, hipStre
 template <typename TIn>
 static int launch_features_t(const VerifyArgs& a, const LargeParams& p, hipStream_t stream) {
   switch (a.dk) {
-    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16>), feat_grid(p, 16, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
-    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32>), feat_grid(p, 32, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
-    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64>), feat_grid(p, 64, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
-    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128>), feat_grid(p, 128, a.dv), dim3(kFT), 0, stream, p, a.dv); break;
+    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16, 0>), feat_grid(p, 16, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
+    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32, 0>), feat_grid(p, 32, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
+    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64, 0>), feat_grid(p, 64, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
+    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128, 0>), feat_grid(p, 128, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
     default: return set_error(GDN_EUNSUPPORTED, "features: dk=%d unsupported", a.dk);
   }
   const hipError_t e = hipGetLastError();
@@ -422,7 +505,7 @@ static int launch_features_t(const VerifyArgs& a, const LargeParams& p, hipStrea
 
 int launch_features(const VerifyArgs& a, float* F, hipStream_t stream) {
   if (a.T > kLMaxT) return set_error(GDN_EUNSUPPORTED, "features: T=%d exceeds %d", a.T, kLMaxT);
-  const LargeParams p = large_params(a, F);
+  const LargeParams p = large_params(a, F, false);
   if (a.in_dtype == GDN_BF16) return launch_features_t<BF16>(a, p, stream);
   return launch_features_t<float>(a, p, stream);
 }
@@ -471,7 +554,7 @@ int launch_verify_noalloc(const VerifyArgs& a, hipStream_t stream) {
   int rc = GDN_OK;
   void* ws = scratch_address(&rc);
   if (!ws) return rc;
-  return launch_verify_large(a, static_cast<float*>(ws), size_t(GDN_NOALLOC_SCRATCH_BYTES), stream);
+  return launch_verify_large(a, ws, size_t(GDN_NOALLOC_SCRATCH_BYTES), stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -16,15 +16,15 @@ static int g_reached = 0;
 namespace gdn {
 int launch_prepare(int, int, const int32_t*, void*, int32_t*, hipStream_t) { return ++g_reached, GDN_OK; }
 int launch_verify(const VerifyArgs&, hipStream_t) { return ++g_reached, GDN_OK; }
-int launch_verify_large(const VerifyArgs&, float*, size_t, hipStream_t) { return ++g_reached, GDN_OK; }
+int launch_verify_large(const VerifyArgs&, void*, size_t, hipStream_t) { return ++g_reached, GDN_OK; }
 int launch_verify_noalloc(const VerifyArgs&, hipStream_t) { return ++g_reached, GDN_OK; }
 int launch_verify_chunked(const VerifyArgs&, void*, size_t, hipStream_t) { return ++g_reached, GDN_OK; }
 int launch_commit(const CommitArgs&, hipStream_t) { return ++g_reached, GDN_OK; }
 size_t large_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
-  return size_t(B) * T * (2 * Hk * dk + Hv * dv) * 4;
+  return ((size_t(B) * T * (2 * Hk * dk + Hv * dv) * 2 + 255) & ~size_t(255)) + size_t(B) * T * Hv * 4;
 }
 size_t chunked_workspace_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
-  return large_workspace_bytes(B, T, Hk, Hv, dk, dv) + size_t(B) * Hv * T * dv * 4;
+  return size_t(B) * T * (2 * Hk * dk + Hv * dv) * 4 + size_t(B) * Hv * T * dv * 4;
 }
 static char g_ws[64];
 void* stream_workspace(size_t, hipStream_t, int* rc) { return *rc = GDN_OK, g_ws; }

@@ -60,8 +60,8 @@ def test_noalloc_matches_verify(G, orc):
 
 def test_noalloc_refuses_oversize(G):
     L = G.lib()
-    d = G.make_dims(8, 512, 16, 48, 128, 128)   # 8 * 512 * 10240 * 4 bytes of features
-    assert 8 * 512 * 10240 * 4 > G.NOALLOC_SCRATCH_BYTES
+    d = G.make_dims(8, 512, 16, 48, 128, 128)   # B T (2 C + 4 Hv) bytes of features, C = 10240
+    assert 8 * 512 * (2 * 10240 + 4 * 48) > G.NOALLOC_SCRATCH_BYTES
     fake = [ctypes.c_void_p(0x1000)] * 10       # never dereferenced: refused on the host
     assert L.gdn_tree_verify_noalloc(ctypes.byref(d), *fake, None) == G.GDN_EUNSUPPORTED
     assert "workspace" in G.last_error()
