@@ -23,9 +23,8 @@
 //                 the power of two that puts its largest magnitude in [1, 2),
 //                 exact, undone on the output), then tiles of 32 positions:
 //                 16 lanes per node walk the paths with the features of the
-//                 path nodes gathered from FH (two steps of loads ahead;
-//                 fp16 operands into fp32 accumulators by mixed-precision
-//                 FMAs), the value heads of one key head on one XCD so that
+//                 path nodes gathered from FH (fp16 operands into fp32
+//                 accumulators by mixed-precision FMAs), the value heads of one key head on one XCD so that
 //                 they share its k~ rows in L2,
 //                 r x -> an fp16 tile, O^T = S0 (r X)^T on
 //                 v_mfma_f32_16x16x32_f16 (fp32 accumulation), plus acc.
@@ -277,7 +276,10 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   for (int j = tid; j < T; j += kLT) {
     const int nd = m.order[bt + j];
     s_ord[j] = int16_t(nd);
-    s_ppos[j] = int16_t(j < nval ? m.ppos[bt + j] : -1);
+    // a parent sits at a smaller position (depth order); anything else
+    // (corrupt metadata) ends the walk, so every walk terminates
+    const int pp = j < nval ? m.ppos[bt + j] : -1;
+    s_ppos[j] = int16_t(pp >= 0 && pp < j ? pp : -1);
     s_al[j] = j < nval ? ld(alpha, (bt + nd) * Hv + h) : 0.0f;
     s_be[j] = j < nval ? ld(beta, (bt + nd) * Hv + h) : 0.0f;
     s_vs[j] = j < nval ? p.Vs[(bt + j) * Hv + h] : 0.0f;
@@ -332,39 +334,26 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 #pragma unroll
         for (int e = 0; e < CK; ++e) x[e] = (float)q0[e];
       }
-      // walk to the root; the path nodes' features load two steps ahead
+      // walk to the root.  The gathers of the path rows are what bounds this
+      // loop (L2 / MALL bandwidth, 16 resident waves per CU hide their
+      // latency): loading rows ahead, which past the root means loading
+      // rows that are never used, measured slower.
       const _Float16* Fk = Fb + nq + g * DK + ln * CK;
       const _Float16* Fv = Fb + 2 * nq + h * DV + ln * CV;
-      int t = pos;
-      int t1 = s_ppos[t];
-      int t2 = t1 >= 0 ? s_ppos[t1] : -1;
-      HK kc = ld_h<CK>(Fk + size_t(t) * C);
-      HVv vc = ld_h<CV>(Fv + size_t(t) * C);
-      const size_t o1 = size_t(t1 >= 0 ? t1 : t) * C;  // clamped: not used past the root
-      HK k1 = ld_h<CK>(Fk + o1);
-      HVv v1 = ld_h<CV>(Fv + o1);
-      while (t >= 0) {  // uniform per 16-lane node group
-        const size_t o2 = size_t(t2 >= 0 ? t2 : t) * C;
-        const HK k2 = ld_h<CK>(Fk + o2);
-        const HVv v2 = ld_h<CV>(Fv + o2);
+      for (int t = pos; t >= 0; t = s_ppos[t]) {  // uniform per 16-lane node group
+        const HK kt = ld_h<CK>(Fk + size_t(t) * C);
+        const HVv vt = ld_h<CV>(Fv + size_t(t) * C);
         float s = 0.0f;
 #pragma unroll
-        for (int e = 0; e < CK; ++e) s = fmaf((float)kc[e], x[e], s);
+        for (int e = 0; e < CK; ++e) s = fmaf((float)kt[e], x[e], s);
         s = group_sum<16>(s);
         const float c = s_be[t] * s;
         const float rc = r * c * s_vs[t];
 #pragma unroll
-        for (int e = 0; e < CV; ++e) acc[e] = fmaf(rc, (float)vc[e], acc[e]);
+        for (int e = 0; e < CV; ++e) acc[e] = fmaf(rc, (float)vt[e], acc[e]);
 #pragma unroll
-        for (int e = 0; e < CK; ++e) x[e] = fmaf(-c, (float)kc[e], x[e]);
+        for (int e = 0; e < CK; ++e) x[e] = fmaf(-c, (float)kt[e], x[e]);
         r *= s_al[t];
-        t = t1;
-        t1 = t2;
-        t2 = t2 >= 0 ? s_ppos[t2] : -1;
-        kc = k1;
-        k1 = k2;
-        vc = v1;
-        v1 = v2;
       }
     }
     // r x -> fp16 tile row jn (zero for padding positions)
