@@ -216,3 +216,34 @@ def test_two_streams_share_nothing(G, orc):
         ref = orc.verify(w)
         got = d.out.cpu().numpy().astype(np.float64)
         assert np.max(np.abs(got - ref)) <= O_TOL * np.max(np.abs(ref))
+
+
+@pytest.mark.parametrize("vscale", [1e5, 1e-6])
+def test_value_range_through_fp16_workspace(G, orc, vscale):
+    """The workspace above 128 slots holds v~ in fp16 with a power-of-two
+    scale per (position, head): raw values (and their conv-state slots)
+    scaled by 1e5 put v~ far above the fp16 range, by 1e-6 below its
+    normal range.  With S0 = 0 the outputs are the value terms alone, so
+    the 2e-3 max|o_ref| bar measures them."""
+    import torch
+    w = W.make_random(9300, 2, 256, 1, 2, 128, 128, "bf16", n_valid=[256, 200], shuffle=True)
+    v = W.bf16_bits_to_f32(w.v).astype(np.float64) * vscale
+    w.v = W.f32_to_bf16_bits(v.astype(np.float32))
+    cs = w.conv_state.copy()
+    cs[:, :, 2 * w.Hk * w.dk:] *= vscale
+    w.conv_state = cs
+    w.S0 = np.zeros_like(w.S0)
+    _announce(f"value range x{vscale:g} through the fp16 workspace (T=256)")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    dt.verify()
+    torch.cuda.synchronize()
+    got = dt.out.cpu().numpy().astype(np.float64)
+    ref = orc.verify(w)
+    assert np.isfinite(got).all()
+    # the post-conv values really leave fp16's normal range (65504 / 2^-14)
+    vt = orc.features(w)[..., 2 * w.Hk * w.dk:][w.parent != W.PAD]
+    assert np.max(np.abs(vt)) > 65504.0 if vscale > 1 else np.max(np.abs(vt)) < 2.0 ** -14
+    err = _out_err(got, ref)
+    _announce(f"  err {err:.3e}  max|o_ref| {np.max(np.abs(ref)):.3e}")
+    assert err <= O_TOL
