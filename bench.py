@@ -451,7 +451,13 @@ def main() -> int:
         out["detail"]["copy_calibration_bytes_each"] = 2 * 4 * n
         del src, dst
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w)
+        cb = cpu_baseline(w)
+        # part of this ratio is algorithmic: the oracle replays the full state
+        # along every path, the GPU path pulls the query back
+        cb["gpu_speedup_vs_naive_replay_oracle"] = {
+            "all_threads": round(out["value"] / cb["value"], 1),
+            "one_thread": round(out["value"] / cb["value_1thread"], 1)}
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
     return 0
 
