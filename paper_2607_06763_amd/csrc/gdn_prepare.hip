@@ -14,20 +14,23 @@
 namespace gdn {
 
 constexpr int kPrepMaxT = 512;
-constexpr int kPrepMaxW = kPrepMaxT / 64;
 
+// KW = ceil(T / 64) ancestor words per node (1, 2, 4 or 8; trees of up to
+// 64 KW slots), a compile-time count so that the rows move as whole vectors
+template <int KW>
 __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __restrict__ parent,
                                                             MetaPtrs m, int32_t* tree_status,
                                                             int T) {
-  __shared__ int s_par[kPrepMaxT];
-  __shared__ int s_nxt[kPrepMaxT];
-  __shared__ __align__(16) int s_dep[kPrepMaxT];
-  __shared__ uint64_t s_anc[kPrepMaxT * kPrepMaxW];
+  constexpr int kMaxT = 64 * KW;
+  __shared__ int s_par[kMaxT];
+  __shared__ int s_nxt[kMaxT];
+  __shared__ __align__(16) int s_dep[kMaxT];
+  __shared__ __align__(16) uint64_t s_anc[kMaxT * KW];
   __shared__ int s_bad, s_roots, s_real, s_cycle;
 
   const int b = blockIdx.x;
   const int i = threadIdx.x;
-  const int W = m.W;
+  const int W = m.W;  // the blob's word count, ceil(T / 64) <= KW
   const bool slot = i < T;
 
   if (i == 0) {
@@ -60,29 +63,27 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
     status = GDN_TREE_MULTI_ROOT;
 
   // pointer jumping (only meaningful for a tree with valid parent values)
-  uint64_t anc[kPrepMaxW];
+  uint64_t anc[KW];
 #pragma unroll
-  for (int w = 0; w < kPrepMaxW; ++w) anc[w] = 0;
+  for (int w = 0; w < KW; ++w) anc[w] = 0;
   int nxt = (real && p >= 0 && status == GDN_TREE_OK) ? p : -1;
   int dep = (nxt >= 0) ? 1 : 0;
 #pragma unroll
-  for (int w = 0; w < kPrepMaxW; ++w)
+  for (int w = 0; w < KW; ++w)
     if (nxt >= 0 && w == (nxt >> 6)) anc[w] |= 1ull << (nxt & 63);
   for (int span = 1; span < T; span <<= 1) {
     if (slot) {
       s_nxt[i] = nxt;
       s_dep[i] = dep;
 #pragma unroll
-      for (int w = 0; w < kPrepMaxW; ++w)
-        if (w < W) s_anc[i * kPrepMaxW + w] = anc[w];
+      for (int w = 0; w < KW; ++w) s_anc[i * KW + w] = anc[w];
     }
     __syncthreads();
     if (nxt >= 0) {
       int j = nxt;
       dep += s_dep[j];
 #pragma unroll
-      for (int w = 0; w < kPrepMaxW; ++w)
-        if (w < W) anc[w] |= s_anc[j * kPrepMaxW + w];
+      for (int w = 0; w < KW; ++w) anc[w] |= s_anc[j * KW + w];
       nxt = s_nxt[j];
     }
     __syncthreads();
@@ -110,11 +111,12 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
     return;
   }
 
-  // canonical order: rank by key (depth, index); padding keyed after all
-  // depths; the keys are read four at a time (slots T .. up to a multiple of
-  // 4 hold a key above every real one, so they never count)
+  // canonical order: rank by (depth, index), padding after all depths, as
+  // the count of smaller keys depth * 1024 + index (distinct; T <= 512);
+  // the keys are read four at a time (slots T .. up to a multiple of 4 hold
+  // a key above every real one, so they never count)
   const int T4 = (T + 3) & ~3;
-  if (i < T4) s_dep[i] = slot ? (real ? dep : T + 1) : 0x7fffffff;
+  if (i < T4) s_dep[i] = slot ? ((real ? dep : T + 1) << 10) | i : 0x7fffffff;
   __syncthreads();
   if (slot) {
     const int key = s_dep[i];
@@ -122,16 +124,15 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
 #pragma unroll 4
     for (int j = 0; j < T4; j += 4) {
       const int4 k4 = *reinterpret_cast<const int4*>(s_dep + j);
-      rank += (k4.x < key) || (k4.x == key && j < i);
-      rank += (k4.y < key) || (k4.y == key && j + 1 < i);
-      rank += (k4.z < key) || (k4.z == key && j + 2 < i);
-      rank += (k4.w < key) || (k4.w == key && j + 3 < i);
+      rank += (k4.x < key) + (k4.y < key) + (k4.z < key) + (k4.w < key);
     }
     m.order[base + rank] = i;
     m.pos[base + i] = rank;
     m.depth[base + i] = real ? dep : -1;
     m.parent[base + i] = p;
-    for (int w = 0; w < W; ++w) m.anc[(size_t(base) + i) * W + w] = real ? anc[w] : 0;
+#pragma unroll
+    for (int w = 0; w < KW; ++w)
+      if (w < W) m.anc[(size_t(base) + i) * W + w] = real ? anc[w] : 0;
     s_nxt[i] = rank;  // position of slot i (s_nxt is free after the jumps)
   }
   __syncthreads();
@@ -152,7 +153,14 @@ int launch_prepare(int B, int T, const int32_t* parent, void* meta, int32_t* tre
   if (T > kPrepMaxT) return set_error(GDN_EUNSUPPORTED, "prepare: T=%d exceeds %d", T, kPrepMaxT);
   MetaPtrs m = meta_ptrs(meta, B, T);
   int threads = ((T + kWave - 1) / kWave) * kWave;
-  hipLaunchKernelGGL(prepare_kernel, dim3(B), dim3(threads), 0, stream, parent, m, tree_status, T);
+  if (m.W <= 1)
+    hipLaunchKernelGGL(prepare_kernel<1>, dim3(B), dim3(threads), 0, stream, parent, m, tree_status, T);
+  else if (m.W <= 2)
+    hipLaunchKernelGGL(prepare_kernel<2>, dim3(B), dim3(threads), 0, stream, parent, m, tree_status, T);
+  else if (m.W <= 4)
+    hipLaunchKernelGGL(prepare_kernel<4>, dim3(B), dim3(threads), 0, stream, parent, m, tree_status, T);
+  else
+    hipLaunchKernelGGL(prepare_kernel<8>, dim3(B), dim3(threads), 0, stream, parent, m, tree_status, T);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "prepare launch: %s", hipGetErrorString(e));
   return GDN_OK;
