@@ -104,6 +104,29 @@ def test_prepare_bit_exact(G, orc, cfg):
     _check_meta(G, dt, w, orc)
 
 
+@pytest.mark.parametrize("T", [1, 63, 64, 65, 128, 129, 192, 193, 256, 257, 320, 384, 448, 511, 512])
+def test_prepare_word_count_boundaries(G, orc, T):
+    """The prepare kernel is built for 1, 2, 4 and 8 ancestor words per node;
+    trees of 129-192 slots use 3 of the 4-word build.  At every boundary: a
+    relabelled random tree, a padded one, a chain (the longest pointer
+    jumping) and a tree with a cycle, bit-exact against the oracle."""
+    rng = np.random.default_rng(4200 + T)
+    par = np.stack([W.random_tree(rng, T, None, True),
+                    W.random_tree(rng, T, T // 2 + 1, True),
+                    W.chain_tree(T),
+                    W.random_tree(rng, T, None, True)])
+    if T >= 4:  # close a cycle among three non-root nodes of the last tree
+        nodes = [i for i in range(T) if par[3, i] != -1][:3]
+        par[3, nodes[0]], par[3, nodes[1]], par[3, nodes[2]] = nodes[1], nodes[2], nodes[0]
+    w = W.make_random(4300 + T, 4, T, 1, 1, 16, 16, "bf16", parent=par)
+    _announce(f"prepare boundaries T={T}")
+    dt = G.DeviceTree(w)
+    dt.prepare()
+    _check_meta(G, dt, w, orc)
+    if T >= 4:
+        assert orc.prepare(w.parent)["status"][3] != 0
+
+
 @pytest.mark.parametrize("cfg", [0, 1, 2, 3])
 def test_verify_named_full(G, orc, cfg):
     w = W.make_config(cfg)
