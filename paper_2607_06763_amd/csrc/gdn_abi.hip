@@ -270,9 +270,11 @@ int gdn_tree_step(const gdn_dims* dims, const void* prev_meta, const int32_t* pr
   a.conv_state_out = conv_state_out;
   a.S = S;
   a.commit_status = commit_status;
-  if (a.T <= kSmallMaxT) return launch_verify(a, stream);
-  // larger trees: the commit kernels (conv state into conv_state_out), then
-  // the verification against the committed state
+  // up to 128 slots the verify kernel commits; above, the pull-back commits
+  // each head's rows (heads of at least 512 state elements)
+  if (a.T <= kSmallMaxT || a.dk * a.dv >= 512) return verify_any(a, stream);
+  // tiny heads above 128 slots: the commit kernels (conv state into
+  // conv_state_out), then the verification against the committed state
   CommitArgs c;
   c.B = a.B;
   c.T = a.T;

@@ -29,9 +29,10 @@
 //                 r x -> an fp16 tile, O^T = S0 (r X)^T on
 //                 v_mfma_f32_16x16x32_f16 (fp32 accumulation), plus acc.
 #include <map>
+#include <type_traits>
 #include <mutex>
 
-#include "gdn_internal.h"
+#include "gdn_commit_rows.h"
 
 namespace gdn {
 
@@ -50,6 +51,9 @@ struct LargeParams {
   float* F;       // fp32 features [B][T][C] (chunked form)
   _Float16* FH;   // fp16 features [B][T][C] (pull-back)
   float* Vs;      // inverse v~ row scales [B][T][Hv] (pull-back)
+  // fused step: the previous step's commit, run by the pull-back on the rows
+  // it reads (conv_state above is then the conv state after the commit)
+  CommitParams cp;
 };
 
 static size_t fh_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
@@ -202,9 +206,12 @@ struct PullSmem {
   static constexpr size_t plane = size_t(DV) * KP * 2;
   static constexpr size_t xt = size_t(kLTile) * KP * 2;
   static constexpr size_t pt = size_t(kLTile) * PP * 4;
+  // the plane and the two tiles; in the fused step the commit's LDS first
+  static constexpr size_t front = plane + xt + pt > commit_lds_bytes<DK, DV>() ? plane + xt + pt
+                                                                              : commit_lds_bytes<DK, DV>();
   static constexpr size_t inv = size_t(DV) * 4;
   static constexpr size_t meta = size_t(kLMaxT) * (2 + 2 + 4 + 4 + 4);
-  static constexpr size_t total = plane + xt + pt + inv + meta;
+  static constexpr size_t total = front + inv + meta;
 };
 
 template <int N>
@@ -236,7 +243,7 @@ __device__ __forceinline__ typename HalfVec<N>::type ld_h(const _Float16* src) {
   return *reinterpret_cast<const typename HalfVec<N>::type*>(src);
 }
 
-template <int DK, int DV, typename TIn>
+template <int DK, int DV, typename TIn, bool FUSED>
 __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   using SM = PullSmem<DK, DV>;
   constexpr int KP = SM::KP, PP = SM::PP;
@@ -246,8 +253,8 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   _Float16* s_plane = reinterpret_cast<_Float16*>(smem);
   _Float16* s_x = reinterpret_cast<_Float16*>(smem + SM::plane);
   float* s_p = reinterpret_cast<float*>(smem + SM::plane + SM::xt);
-  float* s_inv = reinterpret_cast<float*>(smem + SM::plane + SM::xt + SM::pt);
-  int16_t* s_ord = reinterpret_cast<int16_t*>(smem + SM::plane + SM::xt + SM::pt + SM::inv);
+  float* s_inv = reinterpret_cast<float*>(smem + SM::front);
+  int16_t* s_ord = reinterpret_cast<int16_t*>(smem + SM::front + SM::inv);
   int16_t* s_ppos = s_ord + kLMaxT;
   float* s_al = reinterpret_cast<float*>(s_ppos + kLMaxT);
   float* s_be = s_al + kLMaxT;
@@ -284,8 +291,36 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
     s_be[j] = j < nval ? ld(beta, (bt + nd) * Hv + h) : 0.0f;
     s_vs[j] = j < nval ? p.Vs[(bt + j) * Hv + h] : 0.0f;
   }
-  // ---- S0 -> fp16 plane (16 lanes per row), zero columns past DK
-  if (nval > 0) {
+  if constexpr (FUSED) {
+    // ---- fused step: the previous step's accepted path is committed into
+    //      this head's rows (its LDS in the plane and tile region), the rows
+    //      go back to S and straight into the fp16 plane
+    using CS = CommitSplit<DK, DV, kLT>;
+    float srow[CS::EPT];
+    const bool changed = commit_rows<DK, DV, TIn, kLT, true>(p.cp, b, h, tid, commit_lds<DK, DV>(smem), srow);
+    if (changed) store_rows<DK, DV, kLT>(p.cp.S, b, h, Hv, tid, srow);
+    const int row = tid / CS::LPR, col0 = (tid % CS::LPR) * CS::CPT;
+#pragma unroll
+    for (int i = 0; i < CS::R; ++i) {
+      float mx = 0.0f;
+#pragma unroll
+      for (int e = 0; e < CS::CPT; ++e) mx = fmaxf(mx, fabsf(srow[i * CS::CPT + e]));
+      mx = group_max<CS::LPR>(mx);
+      float sc, inv;
+      row_scale(mx, sc, inv);
+      const int r = row + i * CS::RS;
+#pragma unroll
+      for (int e = 0; e < CS::CPT; ++e) s_plane[r * KP + col0 + e] = (_Float16)(srow[i * CS::CPT + e] * sc);
+      if (tid % CS::LPR == 0) s_inv[r] = inv;
+    }
+    if constexpr (DK < 32) {
+      for (int i = tid; i < DV * (32 - DK); i += kLT)
+        s_plane[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
+      for (int i = tid; i < kLTile * (32 - DK); i += kLT)
+        s_x[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
+    }
+  } else if (nval > 0) {
+    // ---- S0 -> fp16 plane (16 lanes per row), zero columns past DK
     const float* S0 = p.S0 + (size_t(b) * Hv + h) * size_t(DV) * DK;
     const int ln = tid & 15;
     for (int r0 = 0; r0 < DV; r0 += kLT / 16) {
@@ -405,29 +440,46 @@ static dim3 feat_grid(const LargeParams& p, int dk, int dv, bool half) {
   return dim3((n4 + kFT - 1) / kFT, (p.T + kFP - 1) / kFP, p.B);
 }
 
-template <int DK, int DV, typename TIn>
-static int launch_large_t(const LargeParams& p, hipStream_t stream) {
-  hipLaunchKernelGGL((feat_kernel<TIn, DK, DV / 4>), feat_grid(p, DK, DV, true), dim3(kFT), 0, stream, p, DV);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
+template <int DK, int DV, typename TIn, bool FUSED>
+static int launch_pull(const LargeParams& p, hipStream_t stream) {
   using SM = PullSmem<DK, DV>;
-  const int rc = ensure_dynamic_lds(reinterpret_cast<const void*>(&pull_kernel<DK, DV, TIn>), int(SM::total),
-                                    "verify (T > 128)");
+  const int rc = ensure_dynamic_lds(reinterpret_cast<const void*>(&pull_kernel<DK, DV, TIn, FUSED>),
+                                    int(SM::total), "verify (T > 128)");
   if (rc != GDN_OK) return rc;
   const int units = p.B * p.Hk, G = p.Hv / p.Hk;
-  hipLaunchKernelGGL((pull_kernel<DK, DV, TIn>), dim3((units + 7) / 8 * 8 * G), dim3(kLT), SM::total, stream, p);
-  e = hipGetLastError();
+  hipLaunchKernelGGL((pull_kernel<DK, DV, TIn, FUSED>), dim3((units + 7) / 8 * 8 * G), dim3(kLT), SM::total,
+                     stream, p);
+  const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) launch: %s", hipGetErrorString(e));
   return GDN_OK;
+}
+
+// fused: the conv-state part of the previous step's commit first (the
+// features read the conv state after it), the state rows inside the
+// pull-back
+template <int DK, int DV, typename TIn>
+static int launch_large_t(const LargeParams& p, bool fused, hipStream_t stream) {
+  constexpr bool kCanFuse = commit_threads(DK, DV) == kLT;
+  if (fused) {
+    if (!kCanFuse) return set_error(GDN_EUNSUPPORTED, "step (T > 128): dk * dv = %d below 512", DK * DV);
+    const int rc = launch_commit_conv(p.cp, DK, DV, std::is_same<TIn, BF16>::value ? GDN_BF16 : GDN_F32, stream);
+    if (rc != GDN_OK) return rc;
+  }
+  hipLaunchKernelGGL((feat_kernel<TIn, DK, DV / 4>), feat_grid(p, DK, DV, true), dim3(kFT), 0, stream, p, DV);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
+  if constexpr (kCanFuse)
+    if (fused) return launch_pull<DK, DV, TIn, true>(p, stream);
+  return launch_pull<DK, DV, TIn, false>(p, stream);
 }
 
 template <int DK, typename TIn>
 static int large_dv(const VerifyArgs& a, const LargeParams& p, hipStream_t s) {
   switch (a.dv) {
-    case 16: return launch_large_t<DK, 16, TIn>(p, s);
-    case 32: return launch_large_t<DK, 32, TIn>(p, s);
-    case 64: return launch_large_t<DK, 64, TIn>(p, s);
-    case 128: return launch_large_t<DK, 128, TIn>(p, s);
+    case 16: return launch_large_t<DK, 16, TIn>(p, a.fused, s);
+    case 32: return launch_large_t<DK, 32, TIn>(p, a.fused, s);
+    case 64: return launch_large_t<DK, 64, TIn>(p, a.fused, s);
+    case 128: return launch_large_t<DK, 128, TIn>(p, a.fused, s);
   }
   return set_error(GDN_EUNSUPPORTED, "verify: dv=%d unsupported", a.dv);
 }
@@ -466,6 +518,26 @@ static LargeParams large_params(const VerifyArgs& a, void* ws, bool half) {
   p.FH = half ? static_cast<_Float16*>(ws) : nullptr;
   p.Vs = half ? reinterpret_cast<float*>(static_cast<unsigned char*>(ws) + fh_bytes(a.B, a.T, a.Hk, a.Hv, a.dk, a.dv))
               : nullptr;
+  p.cp = CommitParams{};
+  if (a.fused) {
+    p.conv_state = a.conv_state_out;  // the features see the committed conv state
+    p.cp.B = a.B;
+    p.cp.T = a.T;
+    p.cp.Hk = a.Hk;
+    p.cp.Hv = a.Hv;
+    p.cp.meta = a.pmeta;
+    p.cp.accepted = a.paccepted;
+    p.cp.q = a.pq;
+    p.cp.k = a.pk;
+    p.cp.v = a.pv;
+    p.cp.alpha = a.palpha;
+    p.cp.beta = a.pbeta;
+    p.cp.conv_w = a.conv_w;
+    p.cp.cs_in = a.conv_state;
+    p.cp.cs_out = a.conv_state_out;
+    p.cp.S = a.S;
+    p.cp.commit_status = a.commit_status;
+  }
   return p;
 }
 

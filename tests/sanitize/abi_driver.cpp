@@ -100,8 +100,14 @@ int main() {
   expect("commit ok", gdn_tree_commit(&ok, p, ci, p, p, p, p, p, f, fo, fo, io, nullptr), GDN_OK, 1);
   expect("step ok", gdn_tree_step(&ok, p, ci, p, p, p, p, p, io, p, p, p, p, p, p, f, f, fo + 2 * 3 * C, fo, fo,
                                   nullptr), GDN_OK, 1);
-  expect("step large ok (commit + verify)",
+  expect("step large ok (fused pull-back)",
          gdn_tree_step(&large, p, ci, p, p, p, p, p, io, p, p, p, p, p, p, f, f, fo + 2 * 3 * C, fo, fo, nullptr),
+         GDN_OK, 1);
+  gdn_dims tiny = large;  // 16 x 16 heads: the commit kernels, then verify
+  tiny.dk = 16;
+  tiny.dv = 16;
+  expect("step large tiny heads (commit + verify)",
+         gdn_tree_step(&tiny, p, ci, p, p, p, p, p, io, p, p, p, p, p, p, f, f, fo + 2 * 3 * C, fo, fo, nullptr),
          GDN_OK, 2);
   if (gdn_tree_meta_bytes(0, 5) != 0 || gdn_tree_meta_bytes(3, 0) != 0 || gdn_tree_meta_bytes(32, 512) % 256) {
     printf("FAIL meta_bytes\n");
