@@ -17,8 +17,10 @@
  * gdn_tree_verify, gdn_tree_verify_noalloc, gdn_tree_verify_chunked and
  * gdn_tree_step all accept 1 <= T <= GDN_MAX_T = 512.  Up to 128 slots verify
  * and step run entirely on chip (step as one fused launch); above 128 they
- * go through a feature workspace (see gdn_tree_verify) and the step runs the
- * commit and the verify as separate launches on the stream.
+ * go through a feature workspace (see gdn_tree_verify), and the step shifts
+ * the conv state, writes the features and then commits each head's state
+ * rows inside the verification launch (heads of dk dv < 512: the commit
+ * kernels, then the verification).
  *
  * Conventions shared by all entry points
  * --------------------------------------
@@ -204,10 +206,12 @@ int gdn_tree_commit(const gdn_dims* dims, const void* meta, const int32_t* accep
 
 /* Fused decode step: the commit of the previous step's accepted node
  * (Sec. 3.4.2) followed by the verification of the current tree (Sec. 3.4,
- * Eq. 7-8) against the state it produces, in one launch.  Results equal
- * gdn_tree_commit(previous step) followed by gdn_tree_verify(current step)
- * with the committed S and conv state; the committed state is formed in
- * registers and verified against without being read back.
+ * Eq. 7-8) against the state it produces, in one launch up to 128 slots
+ * (above: conv-state shift, features, then one launch that commits and
+ * verifies each head).  Results equal gdn_tree_commit(previous step)
+ * followed by gdn_tree_verify(current step) with the committed S and conv
+ * state; the committed state is formed in registers and verified against
+ * without being read back.
  *   prev_meta      meta of the previous step's tree (same B, T)
  *   prev_accepted  int32 [B]: accepted slot of the previous tree, -1 = none
  *   prev_q, prev_k, prev_v, prev_alpha, prev_beta: the previous step's raw

@@ -142,12 +142,14 @@ def test_step_path_lengths(G, orc):
     _check(got, _reference(orc, wp, wc))
 
 
-def test_step_errors(G, orc):
+@pytest.mark.parametrize("T,dk,dv", [(8, 32, 32), (200, 32, 32), (200, 16, 16)])
+def test_step_errors(G, orc, T, dk, dv):
     """Nothing to commit (accepted -1, out of range, padding, invalid previous
     tree) keeps S and copies the conv state; an invalid current tree still
-    commits and gets zero outputs."""
-    T = 8
-    prev = np.array([
+    commits and gets zero outputs.  T = 8: one fused launch; T = 200: the
+    commit inside the pull-back (32 x 32 heads) or the commit kernels before
+    the verification (16 x 16 heads)."""
+    prev8 = np.array([
         [-1, 0, 0, 1, 1, 2, 2, 3],       # accepted -1
         [-1, 0, 0, 1, 1, 2, 2, 3],       # accepted out of range
         [-1, 0, -2, -2, -2, -2, -2, -2],  # accepted padding
@@ -156,11 +158,14 @@ def test_step_errors(G, orc):
         [-1, 0, 0, 1, 1, 2, 2, 3],       # ok, current tree empty
         [-1, 0, 0, 1, 1, 2, 2, 3],       # ok
     ], np.int32)
+    prev = np.full((7, T), W.PAD, np.int32)
+    prev[:, :8] = prev8
     cur = np.array([W.heap_tree(T)] * 7, np.int32)
-    cur[4] = [-1, -1, 0, 1, -2, -2, -2, -2]
-    cur[5] = -2
-    wp, wc = _pair(6700, 7, T, 2, 4, 32, 32, "bf16", prev_parent=prev, cur_parent=cur)
-    wp.accepted[:] = [-1, 8, 3, 3, 7, 5, 6]
+    cur[4] = W.PAD
+    cur[4, :4] = [-1, -1, 0, 1]
+    cur[5] = W.PAD
+    wp, wc = _pair(6700 + T + dk, 7, T, 2, 4, dk, dv, "bf16", prev_parent=prev, cur_parent=cur)
+    wp.accepted[:] = [-1, T, 3, 3, 7, 5, 6]
     got = _run_step(G, wp, wc)
     ref = _reference(orc, wp, wc)
     assert ref[2].tolist() == [0, 5, 5, 3, 0, 0, 0]
