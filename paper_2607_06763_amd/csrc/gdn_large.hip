@@ -210,7 +210,7 @@ struct PullSmem {
   static constexpr size_t front = plane + xt + pt > commit_lds_bytes<DK, DV>() ? plane + xt + pt
                                                                               : commit_lds_bytes<DK, DV>();
   static constexpr size_t inv = size_t(DV) * 4;
-  static constexpr size_t meta = size_t(kLMaxT) * (2 + 2 + 4 + 4 + 4);
+  static constexpr size_t meta = size_t(kLMaxT) * (2 + 4 + 4 + 4 + 4);
   static constexpr size_t total = front + inv + meta;
 };
 
@@ -243,6 +243,13 @@ __device__ __forceinline__ typename HalfVec<N>::type ld_h(const _Float16* src) {
   return *reinterpret_cast<const typename HalfVec<N>::type*>(src);
 }
 
+// the same at a 32-bit byte offset from a wave-uniform base (a scalar base
+// plus a vector offset: no 64-bit address arithmetic per load)
+template <int N>
+__device__ __forceinline__ typename HalfVec<N>::type ld_hb(const _Float16* base, uint32_t byte_off) {
+  return *reinterpret_cast<const typename HalfVec<N>::type*>(reinterpret_cast<const char*>(base) + byte_off);
+}
+
 template <int DK, int DV, typename TIn, bool FUSED>
 __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   using SM = PullSmem<DK, DV>;
@@ -254,11 +261,11 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   _Float16* s_x = reinterpret_cast<_Float16*>(smem + SM::plane);
   float* s_p = reinterpret_cast<float*>(smem + SM::plane + SM::xt);
   float* s_inv = reinterpret_cast<float*>(smem + SM::front);
-  int16_t* s_ord = reinterpret_cast<int16_t*>(smem + SM::front + SM::inv);
-  int16_t* s_ppos = s_ord + kLMaxT;
+  int* s_ppos = reinterpret_cast<int*>(smem + SM::front + SM::inv);
   float* s_al = reinterpret_cast<float*>(s_ppos + kLMaxT);
   float* s_be = s_al + kLMaxT;
   float* s_vs = s_be + kLMaxT;  // inverse v~ row scales by position
+  int16_t* s_ord = reinterpret_cast<int16_t*>(s_vs + kLMaxT);
 
   // Blocks go round-robin over the 8 XCDs: the G value heads of unit u =
   // (sequence, key head), which gather the same k~ rows, take blocks
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
     // a parent sits at a smaller position (depth order); anything else
     // (corrupt metadata) ends the walk, so every walk terminates
     const int pp = j < nval ? m.ppos[bt + j] : -1;
-    s_ppos[j] = int16_t(pp >= 0 && pp < j ? pp : -1);
+    s_ppos[j] = pp >= 0 && pp < j ? pp : -1;
     s_al[j] = j < nval ? ld(alpha, (bt + nd) * Hv + h) : 0.0f;
     s_be[j] = j < nval ? ld(beta, (bt + nd) * Hv + h) : 0.0f;
     s_vs[j] = j < nval ? p.Vs[(bt + j) * Hv + h] : 0.0f;
@@ -373,15 +380,22 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
       // loop (L2 / MALL bandwidth, 16 resident waves per CU hide their
       // latency): loading rows ahead, which past the root means loading
       // rows that are never used, measured slower.
-      const _Float16* Fk = Fb + nq + g * DK + ln * CK;
-      const _Float16* Fv = Fb + 2 * nq + h * DV + ln * CV;
+      // uniform row bases and a 32-bit lane offset (rows of one sequence
+      // span B T C / B < 2^31 halves)
+      const _Float16* Fk = Fb + nq + g * DK;
+      const _Float16* Fv = Fb + 2 * nq + h * DV;
+      const uint32_t Cu = uint32_t(C);
       for (int t = pos; t >= 0; t = s_ppos[t]) {  // uniform per 16-lane node group
-        const HK kt = ld_h<CK>(Fk + size_t(t) * C);
-        const HVv vt = ld_h<CV>(Fv + size_t(t) * C);
-        float s = 0.0f;
+        const uint32_t ro = uint32_t(t) * Cu;  // byte offsets below in 32 bits
+        const HK kt = ld_hb<CK>(Fk, 2 * (ro + uint32_t(ln * CK)));
+        const HVv vt = ld_hb<CV>(Fv, 2 * (ro + uint32_t(ln * CV)));
+        float s0 = 0.0f, s1 = 0.0f;  // two chains
 #pragma unroll
-        for (int e = 0; e < CK; ++e) s = fmaf((float)kt[e], x[e], s);
-        s = group_sum<16>(s);
+        for (int e = 0; e < CK; e += 2) {
+          s0 = fmaf((float)kt[e], x[e], s0);
+          if (e + 1 < CK) s1 = fmaf((float)kt[e + 1], x[e + 1], s1);
+        }
+        const float s = group_sum<16>(s0 + s1);
         const float c = s_be[t] * s;
         const float rc = r * c * s_vs[t];
 #pragma unroll
