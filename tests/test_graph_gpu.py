@@ -31,12 +31,17 @@ def _bits(t):
     return t.view(torch.int32).cpu().numpy()
 
 
-def test_graph_replay_matches_eager(G):
+@pytest.mark.parametrize("T", [40, 200])
+def test_graph_replay_matches_eager(G, T):
+    """Prepare + fused step captured once and replayed three times, each
+    replay bit-identical to the eager sequence.  At T = 200 the step is the
+    conv-state shift, the features and the committing pull-back, through a
+    workspace that an uncaptured call on the capture stream sized first."""
     import torch
-    w = W.make_random(7100, 4, 40, 2, 4, 64, 64, "bf16", shuffle=True)
-    wp = W.make_random(7101, 4, 40, 2, 4, 64, 64, "bf16", shuffle=True)
+    w = W.make_random(7100 + T, 4, T, 2, 4, 64, 64, "bf16", shuffle=True)
+    wp = W.make_random(7101 + T, 4, T, 2, 4, 64, 64, "bf16", shuffle=True)
     wp.conv_w = w.conv_w
-    print("[gpu] graph replay B=4 T=40 Hk=2 Hv=4 d=64", flush=True)
+    print(f"[gpu] graph replay B=4 T={T} Hk=2 Hv=4 d=64", flush=True)
     dp, dc = G.DeviceTree(wp), G.DeviceTree(w)
     dp.prepare()
 
@@ -70,7 +75,7 @@ def test_graph_replay_matches_eager(G):
     cap["cs"].copy_(dp.conv_state)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
+    with torch.cuda.graph(g, stream=side):
         one_step(cap)
     # capturing does not run the kernels: the state is still the initial one
     torch.cuda.synchronize()
