@@ -24,10 +24,15 @@
 //                 exact, undone on the output), then tiles of 32 positions:
 //                 16 lanes per node walk the paths with the features of the
 //                 path nodes gathered from FH (fp16 operands into fp32
-//                 accumulators by mixed-precision FMAs), the value heads of one key head on one XCD so that
-//                 they share its k~ rows in L2,
-//                 r x -> an fp16 tile, O^T = S0 (r X)^T on
+//                 accumulators by mixed-precision FMAs), the value heads of
+//                 one key head on one XCD so that they share its k~ rows in
+//                 L2, r x -> an fp16 tile, O^T = S0 (r X)^T on
 //                 v_mfma_f32_16x16x32_f16 (fp32 accumulation), plus acc.
+// The fused decode step (Sec. 3.4.2) runs the conv-state shift of the
+// previous step's commit first, the features on the committed conv state,
+// and pull_kernel<..., FUSED>, which commits the previous accepted path into
+// its head's state rows (commit_rows) and converts the committed rows
+// straight into its plane.
 #include <map>
 #include <type_traits>
 #include <mutex>
