@@ -216,10 +216,20 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   }
   if (nval > 0) {
     const float* S0 = p.S0 + (size_t(b) * Hv + h) * size_t(DV) * DK;
-    for (int i = tid; i < DV * DK / 4; i += kHT) {
-      const int r = i / (DK / 4), c4 = i % (DK / 4);
-      st_split4(s_s0h + r * LKH + 4 * c4, s_s0l + r * LKH + 4 * c4,
-                *reinterpret_cast<const float4*>(S0 + size_t(r) * DK + 4 * c4));
+    constexpr int NS4 = (DV * DK / 4 + kHT - 1) / kHT;  // float4 per thread, all in flight
+    float4 sv[NS4];
+#pragma unroll
+    for (int j = 0; j < NS4; ++j) {
+      const int i = j * kHT + tid < DV * DK / 4 ? j * kHT + tid : 0;
+      sv[j] = *reinterpret_cast<const float4*>(S0 + size_t(i / (DK / 4)) * DK + 4 * (i % (DK / 4)));
+    }
+#pragma unroll
+    for (int j = 0; j < NS4; ++j) {
+      const int i = j * kHT + tid;
+      if (i < DV * DK / 4) {
+        const int r = i / (DK / 4), c4 = i % (DK / 4);
+        st_split4(s_s0h + r * LKH + 4 * c4, s_s0l + r * LKH + 4 * c4, sv[j]);
+      }
     }
     if constexpr (DK < KP) {  // zero padding of the contraction
       for (int i = tid; i < DV * (KP - DK); i += kHT) {
@@ -236,24 +246,61 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   __syncthreads();
 
   const int NB = (T + kBc - 1) / kBc, NBv = (nval + kBc - 1) / kBc;
-  // block rows of q~ and k~ (zero past the tree) -> hi / lo planes
-  auto load_qk = [&](int jb) {
-    for (int i = tid; i < 2 * kBc * (DK / 4); i += kHT) {
+  // block rows of q~ and k~ (zero past the tree) -> hi / lo planes: the
+  // loads of a block go to registers first (all in flight together, issued
+  // a block ahead where the planes are still in use), then to the planes
+  constexpr int NQK = (2 * kBc * (DK / 4) + kHT - 1) / kHT;
+  float4 qkv[NQK];
+  auto fetch_qk = [&](int jb) {
+#pragma unroll
+    for (int j = 0; j < NQK; ++j) {
+      const int i = j * kHT + tid;
       const int part = i / (kBc * (DK / 4)), rem = i % (kBc * (DK / 4));
       const int r = rem / (DK / 4), c4 = rem % (DK / 4);
       const int pos = kBc * jb + r;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (pos < nval) v = *reinterpret_cast<const float4*>(Fb + pos * C + (part ? nq : 0) + g * DK + 4 * c4);
-      st_split4((part ? s_kh : s_qh) + r * LKH + 4 * c4, (part ? s_kl : s_ql) + r * LKH + 4 * c4, v);
+      // clamped rows: every load is unconditional; rows past the tree are
+      // zeroed at the store
+      const int pc = pos < nval ? pos : 0;
+      qkv[j] = *reinterpret_cast<const float4*>(Fb + pc * C + (part ? nq : 0) + g * DK + 4 * c4);
+    }
+  };
+  auto store_qk = [&](int jb) {
+#pragma unroll
+    for (int j = 0; j < NQK; ++j) {
+      const int i = j * kHT + tid;
+      if (i < 2 * kBc * (DK / 4)) {
+        const int part = i / (kBc * (DK / 4)), rem = i % (kBc * (DK / 4));
+        const int r = rem / (DK / 4), c4 = rem % (DK / 4);
+        const float4 v = kBc * jb + r < nval ? qkv[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+        st_split4((part ? s_kh : s_qh) + r * LKH + 4 * c4, (part ? s_kl : s_ql) + r * LKH + 4 * c4, v);
+      }
     }
   };
 
   // ---- phase A: a Q S0^T -> out, beta (V - a K S0^T) -> U
+  constexpr int NTA = (2 * NTILE + kHT / 64 - 1) / (kHT / 64);  // tasks per wave
+  if (NBv > 0) fetch_qk(0);
   for (int jb = 0; jb < NB; ++jb) {
     if (jb < NBv) {
-      load_qk(jb);
+      store_qk(jb);
       __syncthreads();
-      for (int task = wave; task < 2 * NTILE; task += kHT / 64) {
+      if (jb + 1 < NBv) fetch_qk(jb + 1);  // in flight during this block's products
+      // the value operands of this wave's K S0^T tasks, loaded ahead
+      float vop[NTA][4];
+#pragma unroll
+      for (int ta = 0; ta < NTA; ++ta) {
+        const int task = wave + ta * (kHT / 64);
+        const int t = task % NTILE, ti = t / NTV, tj = t % NTV, col = 16 * tj + (lane & 15);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int pos = kBc * jb + 16 * ti + 4 * (lane >> 4) + r;
+          vop[ta][r] = Fb[(pos < nval ? pos : 0) * C + 2 * nq + h * DV + col];
+        }
+      }
+#pragma unroll
+      for (int ta = 0; ta < NTA; ++ta) {
+        const int task = wave + ta * (kHT / 64);
+        if (task >= 2 * NTILE) continue;  // uniform per wave
         const int kind = task / NTILE, t = task % NTILE;
         const int ti = t / NTV, tj = t % NTV;
         const f32x4 acc = mm16x3<KP>((kind ? s_kh : s_qh) + 16 * ti * LKH, (kind ? s_kl : s_ql) + 16 * ti * LKH,
@@ -268,8 +315,7 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
           if (kind == 0) {
             outb[size_t(s_ord[pos]) * Hv * DV + col] = real ? a * acc[r] : 0.0f;
           } else {
-            const float v = real ? Fb[pos * C + 2 * nq + h * DV + col] : 0.0f;
-            Ub[size_t(pos) * DV + col] = real ? s_be[pos] * (v - a * acc[r]) : 0.0f;
+            Ub[size_t(pos) * DV + col] = real ? s_be[pos] * (vop[ta][r] - a * acc[r]) : 0.0f;
           }
         }
       }
@@ -290,8 +336,9 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   }
 
   // ---- phase B: forward substitution over the blocks
+  if (NBv > 0) fetch_qk(0);
   for (int jb = 0; jb < NBv; ++jb) {
-    load_qk(jb);
+    store_qk(jb);
     for (int i = tid; i < kBc * kHW; i += kHT) {
       const int r = i / kHW, w = i % kHW;
       const int pos = kBc * jb + r;
@@ -438,6 +485,9 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
       }
     }
     __syncthreads();
+    // this block's q / k planes are read for the last time above: the next
+    // block's rows load during the inverse
+    if (jb + 1 < NBv) fetch_qk(jb + 1);
     // ---- (I + X_jj)^-1 = (I + A)(I + A^2)(I + A^4)(I + A^8)(I + A^16):
     //      round s: waves 0-3 square the power of A, waves 4-7 multiply the
     //      partial product by (I + the power formed in round s - 1)
