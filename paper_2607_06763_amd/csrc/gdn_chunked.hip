@@ -283,7 +283,6 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   for (int jb = 0; jb < NB; ++jb) {
     if (jb < NBv) {
       store_qk(jb);
-      __syncthreads();
       if (jb + 1 < NBv) fetch_qk(jb + 1);  // in flight during this block's products
       // the value operands of this wave's K S0^T tasks, loaded ahead
       float vop[NTA][4];
@@ -297,6 +296,7 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
           vop[ta][r] = Fb[(pos < nval ? pos : 0) * C + 2 * nq + h * DV + col];
         }
       }
+      __syncthreads();
 #pragma unroll
       for (int ta = 0; ta < NTA; ++ta) {
         const int task = wave + ta * (kHT / 64);
@@ -336,30 +336,57 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
   }
 
   // ---- phase B: forward substitution over the blocks
-  if (NBv > 0) fetch_qk(0);
+  // block-top inputs of block jb (the ancestor words of its rows, R_j and
+  // the a Q S0^T part of O_j from phase A), loaded a block ahead: every load
+  // is unconditional (clamped rows), padding is zeroed when they are used
+  constexpr int NAW = (kBc * kHW + kHT - 1) / kHT;
+  uint64_t awpf[NAW];
+  f32x4 rrpf[2], oopf[2];
+  auto fetch_top = [&](int jb) {
+#pragma unroll
+    for (int j = 0; j < NAW; ++j) {
+      const int i = j * kHT + tid;
+      const int r = (i / kHW) % kBc, w = i % kHW;
+      const int pos = kBc * jb + r;
+      awpf[j] = m.anc[(bt + s_ord[pos < nval ? pos : 0]) * W + (w < W ? w : 0)];
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = (wave + 8 * u) % NTILE;
+      const int ti = t / NTV, tj = t % NTV, col = 16 * tj + (lane & 15);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int pos = kBc * jb + 16 * ti + 4 * (lane >> 4) + r;
+        const int pc = pos < nval ? pos : 0;
+        rrpf[u][r] = Ub[size_t(pc) * DV + col];
+        oopf[u][r] = outb[size_t(s_ord[pc]) * Hv * DV + col];
+      }
+    }
+  };
+  if (NBv > 0) {
+    fetch_qk(0);
+    fetch_top(0);
+  }
   for (int jb = 0; jb < NBv; ++jb) {
     store_qk(jb);
-    for (int i = tid; i < kBc * kHW; i += kHT) {
-      const int r = i / kHW, w = i % kHW;
-      const int pos = kBc * jb + r;
-      s_anc[i] = (pos < nval && w < W) ? m.anc[(bt + s_ord[pos]) * W + w] : 0ull;
+#pragma unroll
+    for (int j = 0; j < NAW; ++j) {
+      const int i = j * kHT + tid;
+      if (i < kBc * kHW) {
+        const int r = i / kHW, w = i % kHW;
+        s_anc[i] = (kBc * jb + r < nval && w < W) ? awpf[j] : 0ull;
+      }
     }
     f32x4 rr[2], oo[2];  // R_j and O_j tiles of this wave: t = wave, wave + 8
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      rr[u] = zero4();
-      oo[u] = zero4();
       const int t = wave + 8 * u;
-      if (t < NTILE) {
-        const int ti = t / NTV, tj = t % NTV, col = 16 * tj + (lane & 15);
+      const int ti = (t % NTILE) / NTV;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int pos = kBc * jb + 16 * ti + 4 * (lane >> 4) + r;
-          if (pos < nval) {
-            rr[u][r] = Ub[size_t(pos) * DV + col];
-            oo[u][r] = outb[size_t(s_ord[pos]) * Hv * DV + col];
-          }
-        }
+      for (int r = 0; r < 4; ++r) {
+        const bool live = t < NTILE && kBc * jb + 16 * ti + 4 * (lane >> 4) + r < nval;
+        rr[u][r] = live ? rrpf[u][r] : 0.0f;
+        oo[u][r] = live ? oopf[u][r] : 0.0f;
       }
     }
     __syncthreads();
@@ -486,8 +513,11 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
     }
     __syncthreads();
     // this block's q / k planes are read for the last time above: the next
-    // block's rows load during the inverse
-    if (jb + 1 < NBv) fetch_qk(jb + 1);
+    // block's rows and block-top inputs load during the inverse
+    if (jb + 1 < NBv) {
+      fetch_qk(jb + 1);
+      fetch_top(jb + 1);
+    }
     // ---- (I + X_jj)^-1 = (I + A)(I + A^2)(I + A^4)(I + A^8)(I + A^16):
     //      round s: waves 0-3 square the power of A, waves 4-7 multiply the
     //      partial product by (I + the power formed in round s - 1)
