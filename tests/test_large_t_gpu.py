@@ -174,6 +174,7 @@ def _step_check(G, orc, wp, wc):
     (2, 256, 2, 4, 128, 128, "bf16", [256, 180], None),
     (3, 512, 1, 3, 64, 32, "bf16", [512, 0, 400], None),  # includes an empty tree
     (2, 200, 2, 4, 16, 32, "f32", [200, 150], 6),        # one state element per thread
+    (3, 160, 1, 1, 32, 16, "bf16", [160, 1, 129], None),  # 32 lanes per state row, one-node tree
     (2, 300, 1, 2, 16, 16, "bf16", [300, 257], None),    # tiny heads: commit kernels first
 ])
 def test_large_step(G, orc, shape):
