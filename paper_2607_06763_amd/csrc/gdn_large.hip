@@ -209,7 +209,7 @@ struct PullSmem {
   static constexpr int KP = (DK < 32 ? 32 : DK) + 8;  // fp16 row (zero beyond DK)
   static constexpr int PP = DV + 4;                    // fp32 row of the product tile
   static constexpr size_t plane = size_t(DV) * KP * 2;
-  static constexpr size_t xt = size_t(kLTile) * KP * 2;
+  static constexpr size_t xt = size_t(2) * kLTile * KP * 2;  // r x as fp16 hi and lo planes
   static constexpr size_t pt = size_t(kLTile) * PP * 4;
   // the plane and the two tiles; in the fused step the commit's LDS first
   static constexpr size_t front = plane + xt + pt > commit_lds_bytes<DK, DV>() ? plane + xt + pt
@@ -263,7 +263,7 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
   constexpr int KS = (DK < 32 ? 32 : DK) / 32;
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16* s_plane = reinterpret_cast<_Float16*>(smem);
-  _Float16* s_x = reinterpret_cast<_Float16*>(smem + SM::plane);
+  _Float16* s_x = reinterpret_cast<_Float16*>(smem + SM::plane);  // [2][kLTile][KP]: hi, lo
   float* s_p = reinterpret_cast<float*>(smem + SM::plane + SM::xt);
   float* s_inv = reinterpret_cast<float*>(smem + SM::front);
   int* s_ppos = reinterpret_cast<int*>(smem + SM::front + SM::inv);
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
     if constexpr (DK < 32) {
       for (int i = tid; i < DV * (32 - DK); i += kLT)
         s_plane[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
-      for (int i = tid; i < kLTile * (32 - DK); i += kLT)
+      for (int i = tid; i < 2 * kLTile * (32 - DK); i += kLT)
         s_x[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
     }
   } else if (nval > 0) {
@@ -354,7 +354,7 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
     if constexpr (DK < 32) {
       for (int i = tid; i < DV * (32 - DK); i += kLT)
         s_plane[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
-      for (int i = tid; i < kLTile * (32 - DK); i += kLT)
+      for (int i = tid; i < 2 * kLTile * (32 - DK); i += kLT)
         s_x[(i / (32 - DK)) * KP + DK + i % (32 - DK)] = (_Float16)0.0f;
     }
   }
@@ -410,9 +410,17 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
         r *= s_al[t];
       }
     }
-    // r x -> fp16 tile row jn (zero for padding positions)
+    // r x -> tile row jn (zero for padding positions) as fp16 hi + lo: the
+    // product takes both, so x contributes no rounding beyond ~2^-22 (with
+    // fp16 features the key dims are short, and an x rounded once to 11 bits
+    // cost up to 3e-4 of max|o| on 16-dim heads)
 #pragma unroll
-    for (int e = 0; e < CK; ++e) s_x[jn * KP + ln * CK + e] = (_Float16)(r * x[e]);
+    for (int e = 0; e < CK; ++e) {
+      const float rx = r * x[e];
+      const _Float16 hi = (_Float16)rx;
+      s_x[jn * KP + ln * CK + e] = hi;
+      s_x[(kLTile + jn) * KP + ln * CK + e] = (_Float16)(rx - (float)hi);
+    }
     __syncthreads();
     // O^T tiles (16 value rows x 16 positions), K = key channels
     {
@@ -424,7 +432,9 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
         for (int ks = 0; ks < KS; ++ks) {
           const f16x8 a = *reinterpret_cast<const f16x8*>(s_plane + (16 * rt + l16) * KP + 32 * ks + 8 * lg);
           const f16x8 bx = *reinterpret_cast<const f16x8*>(s_x + (16 * ct + l16) * KP + 32 * ks + 8 * lg);
+          const f16x8 bl = *reinterpret_cast<const f16x8*>(s_x + (kLTile + 16 * ct + l16) * KP + 32 * ks + 8 * lg);
           acc4 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bx, acc4, 0, 0, 0);
+          acc4 = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, bl, acc4, 0, 0, 0);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

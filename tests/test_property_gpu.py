@@ -69,6 +69,7 @@ def _ex(B, T, Hk, ratio, dk, dv, dtype, back, fracs, seed):
 @_ex(1, 128, 2, 1, 128, 16, "bf16", 2, [1.0, 1.0, 1.0], 13)      # deep, last on-chip size
 @_ex(2, 1, 1, 3, 32, 64, "f32", 600, [1.0, 0.0, 1.0], 14)        # single node
 @_ex(3, 333, 2, 2, 64, 32, "bf16", 4, [0.6, 0.9, 0.3], 15)       # deep-ish, ragged blocks
+@_ex(1, 200, 2, 3, 16, 16, "f32", 1, [0.0, 0.0, 0.0], 56028726)  # one-node trees, 16-dim heads, fp16 workspace
 def test_property_verify_commit_step(G, orc, s):
     import torch
     B, T = s["B"], s["T"]
