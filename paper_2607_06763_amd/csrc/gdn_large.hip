@@ -8,7 +8,7 @@
 // gives o_i = scale (S0 (r x) + acc) in the stored orientation.  With up to
 // 512 slots the post-conv features of a tree no longer fit in LDS, so the
 // work is split in two launches:
-//   feat_kernel   one workgroup per (1024 channels, 32 positions, sequence):
+//   feat_kernel   one workgroup per (2048 channels, 32 positions, sequence):
 //                 the width-4 conv along each node's path (conv-state slots
 //                 above the root), SiLU, and the per-head L2 norm of q and
 //                 k; written to a workspace of fp16 features FH[B][T][C]
@@ -75,30 +75,101 @@ size_t features_f32_bytes(int B, int T, int Hk, int Hv, int dk, int dv) {
 
 // ---------------------------------------------------------------------------
 // Features: conv taps along the path, SiLU, L2 norm (q, k).  One workgroup
-// per (1024 channels, block of kFP positions, sequence): each thread keeps
-// the conv weights of its 4 channels in registers, the blocks' conv taps are
-// resolved once into LDS, and the raw rows of kFU positions are loaded
-// before any of them is used.
+// per (kFT CPT channels, block of kFP positions, sequence): each thread keeps
+// the conv weights of its CPT channels in registers, the block's conv taps
+// are resolved once into LDS, and the raw rows of the next positions are in
+// flight while the current ones are computed.  CPT = 8 channels per thread
+// for the fp16 workspace (one 16-byte row load and store per tap and
+// position), 4 for the fp32 features, whose 16-byte stores then stay
+// contiguous across the lanes.
 // ---------------------------------------------------------------------------
 constexpr int kFP = 32;  // positions per feature workgroup
-constexpr int kFU = 4;   // positions whose loads are in flight together
 
-// First thread (in units of 4 channels) of the value channels.  For the
-// fp16 features the value heads start on a 32-lane boundary, so that the
-// DV / 4 lanes of each head are aligned consecutive lanes (one row max).
-__host__ __device__ inline int feat_vbase4(int Hk, int dk, bool half) {
-  const int nqk4 = 2 * Hk * dk / 4;
-  return half ? (nqk4 + 31) & ~31 : nqk4;
+// First thread (in units of CPT channels) of the value channels: the q / k
+// threads come first, the value threads start on a wave boundary, so that
+// every wave reads rows of one row stride (the q and k rows have Hk dk
+// elements, the v rows Hv dv) and the dv / CPT lanes of a value head are
+// aligned consecutive lanes of one wave.
+__host__ __device__ inline int feat_vbase(int Hk, int dk, int cpt) {
+  const int nqk = 2 * Hk * dk / cpt;
+  return (nqk + 63) & ~63;
 }
 
-// VG = 0: fp32 features into p.F; VG = DV / 4: fp16 features into p.FH
+// N raw channels of one row (N = 4 or 8), kept as loaded until they are used
+template <typename TIn, int N>
+struct RawRow;
+template <int N>
+struct RawRow<BF16, N> {
+  uint32_t u[N / 2];
+  __device__ __forceinline__ void load(const BF16* p) {
+    if constexpr (N == 8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(p);
+      u[0] = v.x, u[1] = v.y, u[2] = v.z, u[3] = v.w;
+    } else {
+      const uint2 v = *reinterpret_cast<const uint2*>(p);
+      u[0] = v.x, u[1] = v.y;
+    }
+  }
+  __device__ __forceinline__ void get(float (&x)[N]) const {
+#pragma unroll
+    for (int j = 0; j < N / 2; ++j) {
+      x[2 * j] = __uint_as_float(u[j] << 16);
+      x[2 * j + 1] = __uint_as_float(u[j] & 0xffff0000u);
+    }
+  }
+};
+template <int N>
+struct RawRow<float, N> {
+  float4 a[N / 4];
+  __device__ __forceinline__ void load(const float* p) {
+#pragma unroll
+    for (int h = 0; h < N / 4; ++h) a[h] = reinterpret_cast<const float4*>(p)[h];
+  }
+  __device__ __forceinline__ void get(float (&x)[N]) const {
+#pragma unroll
+    for (int h = 0; h < N / 4; ++h) x[4 * h] = a[h].x, x[4 * h + 1] = a[h].y, x[4 * h + 2] = a[h].z, x[4 * h + 3] = a[h].w;
+  }
+};
+
+// Largest |x| over aligned groups of N lanes, on the bit patterns of the
+// magnitudes (the same order as the floats; a NaN counts as 0, as fmaxf
+// would skip it), one DPP max per step.
+template <int N>
+__device__ __forceinline__ float group_absmax(float v) {
+  uint32_t u = __float_as_uint(v) & 0x7fffffffu;
+  u = u > 0x7f800000u ? 0u : u;
+  auto mx = [&](uint32_t a, uint32_t o) { return a > o ? a : o; };
+  if constexpr (N >= 2) u = mx(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), kDppQuadXor1, 0xF, 0xF, false)));
+  if constexpr (N >= 4) u = mx(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), kDppQuadXor2, 0xF, 0xF, false)));
+  if constexpr (N >= 8) u = mx(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), kDppRowHalfMirror, 0xF, 0xF, false)));
+  if constexpr (N >= 16) u = mx(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), kDppRowMirror, 0xF, 0xF, false)));
+  if constexpr (N >= 32) u = mx(u, uint32_t(__shfl_xor(int(u), 16)));
+  static_assert(N <= 32, "group size");
+  return __uint_as_float(u);
+}
+
+// VG = 0: fp32 features into p.F; VG = DV / CPT: fp16 features into p.FH
 // with the v~ rows of each head scaled (inverse scales into p.Vs).
-template <typename TIn, int DK, int VG>
-__global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
+template <typename TIn, int DK, int VG, int CPT>
+__global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV, int ncb) {
   constexpr bool kHalf = VG > 0;
+  static_assert(CPT == 4 || CPT == 8, "channels per thread");
+  // positions per register buffer: 32 registers of raw rows (4 taps each)
+  constexpr int kFU = 32 / (int(sizeof(TIn)) * CPT);
   __shared__ int s_tap[kFP][4];  // node of each tap, or -1 - conv-state slot
-  const int b = blockIdx.z, tid = threadIdx.x;
-  const int p0 = blockIdx.y * kFP;
+  // Blocks go round-robin over the 8 XCDs.  The grid is one-dimensional and
+  // renumbered so that each XCD takes a contiguous range of (position block,
+  // channel block, sequence) in that order: the position blocks of one
+  // channel block of a sequence run on one XCD, where the rows that some of
+  // them load are still in L2 when others gather them as ancestor taps
+  // (measured: 1.5x fewer HBM bytes fetched).
+  const int nblk = gridDim.x, per = nblk / 8;
+  const int id = blockIdx.x;
+  const int L = id < 8 * per ? (id % 8) * per + id / 8 : id;
+  const int nyb = (p.T + kFP - 1) / kFP;
+  const int yb = L % nyb, bx = (L / nyb) % ncb, b = L / (nyb * ncb);
+  const int tid = threadIdx.x;
+  const int p0 = yb * kFP;
   const int T = p.T, Hk = p.Hk, Hv = p.Hv;
   const MetaPtrs m = meta_ptrs(p.meta, p.B, T);
   const int nval = m.status[b] == GDN_TREE_OK ? m.nvalid[b] : 0;
@@ -119,85 +190,136 @@ __global__ __launch_bounds__(kFT) void feat_kernel(LargeParams p, int DV) {
   }
   const int nq = Hk * DK;
   const int C = 2 * nq + Hv * DV;
-  const int vb4 = feat_vbase4(Hk, DK, kHalf);
-  const int c4 = blockIdx.x * kFT + tid;
-  const bool isv = c4 >= vb4;
-  const bool ok = isv ? c4 - vb4 < Hv * DV / 4 : c4 < 2 * nq / 4;
-  const int c = ok ? (isv ? 2 * nq + 4 * (c4 - vb4) : 4 * c4) : 0;
-  // this thread's channels: source tensor, row stride and offset
+  const int vb = feat_vbase(Hk, DK, CPT);
+  const int nqkt = 2 * nq / CPT, nvt = Hv * DV / CPT;
+  const int ct = bx * kFT + tid;
+  const bool isv = ct >= vb;  // the same for the whole wave
+  const bool ok = isv ? ct - vb < nvt : ct < nqkt;
+  // this thread's first channel; lanes past the channels of their kind
+  // compute on the last group of that kind (in bounds) and store nothing
+  const int c = isv ? 2 * nq + CPT * (ct - vb < nvt ? ct - vb : nvt - 1) : CPT * (ct < nqkt ? ct : nqkt - 1);
   const TIn* src;
-  size_t stride;
   int off;
   if (c < nq) {
-    src = static_cast<const TIn*>(p.q), stride = nq, off = c;
+    src = static_cast<const TIn*>(p.q), off = c;
   } else if (c < 2 * nq) {
-    src = static_cast<const TIn*>(p.k), stride = nq, off = c - nq;
+    src = static_cast<const TIn*>(p.k), off = c - nq;
   } else {
-    src = static_cast<const TIn*>(p.v), stride = size_t(Hv) * DV, off = c - 2 * nq;
+    src = static_cast<const TIn*>(p.v), off = c - 2 * nq;
   }
-  src += bt * stride + off;
-  const float* cs = p.conv_state + size_t(b) * 3 * C + c;
-  const float4* wr = reinterpret_cast<const float4*>(p.conv_w + size_t(c) * 4);
-  const float4 w0 = wr[0], w1 = wr[1], w2 = wr[2], w3 = wr[3];
-  const bool qk = c < 2 * nq;
+  // row stride of this wave's tensor (wave-uniform: node offsets are scalar)
+  const int rs = __builtin_amdgcn_readfirstlane(isv ? Hv * DV : nq);
+  src += bt * size_t(rs) + off;
+  float4 wv[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) wv[j] = reinterpret_cast<const float4*>(p.conv_w + size_t(c) * 4)[j];
+  const bool qk = !isv;
+  // the conv-state slots of this thread's channels (taps above the root),
+  // kept in LDS: read under a branch, an LDS load does not make the row
+  // loads in flight wait
+  __shared__ float4 s_cs[3][CPT / 4][kFT];
+  {
+    const float* cs = p.conv_state + size_t(b) * 3 * C + c;
+#pragma unroll
+    for (int sl = 0; sl < 3; ++sl)
+#pragma unroll
+      for (int h = 0; h < CPT / 4; ++h) s_cs[sl][h][tid] = ld4(cs + size_t(sl) * C + 4 * h);
+  }
   float* dst = kHalf ? nullptr : p.F + (bt + p0) * size_t(C) + c;
   _Float16* dsth = kHalf ? p.FH + (bt + p0) * size_t(C) + c : nullptr;
   // the first lane of each value head writes the head's inverse scale
-  const bool vs_lane = kHalf && ok && isv && (c4 - vb4) % (kHalf ? VG : 1) == 0;
-  float* vs = vs_lane ? p.Vs + (bt + p0) * size_t(Hv) + (c4 - vb4) / (kHalf ? VG : 1) : nullptr;
+  const bool vs_lane = kHalf && ok && isv && (ct - vb) % (kHalf ? VG : 1) == 0;
+  float* vs = vs_lane ? p.Vs + (bt + p0) * size_t(Hv) + (ct - vb) / (kHalf ? VG : 1) : nullptr;
   __syncthreads();
-  // the three conv-state slots of this thread's channels (the same for every
-  // position): loaded once, so that every tap below is one unconditional
-  // row load and a select (a load under a branch waits for itself)
-  const float4 cs0 = ld4(cs), cs1 = ld4(cs + C), cs2 = ld4(cs + 2 * size_t(C));
-  // tap value: the loaded row, or for a tap above the root (code -1 - slot)
-  // the conv-state slot
-  auto pick = [&](const float4& raw, int code) {
-    const float4 c = code == -1 ? cs0 : (code == -2 ? cs1 : cs2);
-    return code >= 0 ? raw : c;
-  };
-  for (int i0 = 0; i0 < np; i0 += kFU) {
-    float4 xr[kFU][4];
-    int code[kFU][3];
+  // Two register buffers of kFU positions each: the rows of the next group
+  // are in flight while the current one is computed.  Group indices past
+  // the block are clamped to its last position (loaded again, not stored).
+  RawRow<TIn, CPT> ra[kFU][4], rb[kFU][4];
+  int ca[kFU], cb[kFU];  // tap 0's code: negative iff the position is within 3 of the root
+  auto load_group = [&](RawRow<TIn, CPT> (&xr)[kFU][4], int (&code)[kFU], int g0) {
 #pragma unroll
     for (int u = 0; u < kFU; ++u) {
-      const int i = i0 + u < np ? i0 + u : np - 1;
+      const int i = g0 + u < np ? g0 + u : np - 1;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const int nd = s_tap[i][w];
-        if (w < 3) code[u][w] = nd;
-        xr[u][w] = ld4(src + size_t(nd >= 0 ? nd : 0) * stride);
+        const int nd = __builtin_amdgcn_readfirstlane(s_tap[i][w]);
+        if (w == 0) code[u] = nd;
+        xr[u][w].load(src + (nd >= 0 ? nd : 0) * rs);
       }
     }
+  };
+  auto compute_group = [&](const RawRow<TIn, CPT> (&xr)[kFU][4], const int (&code)[kFU], int g0) {
 #pragma unroll
     for (int u = 0; u < kFU; ++u) {
-      const float4 x[4] = {pick(xr[u][0], code[u][0]), pick(xr[u][1], code[u][1]), pick(xr[u][2], code[u][2]),
-                           xr[u][3]};  // tap 3 is the node itself
-      float y[4];
-      y[0] = silu(fmaf(w0.w, x[3].x, fmaf(w0.z, x[2].x, fmaf(w0.y, x[1].x, w0.x * x[0].x))));
-      y[1] = silu(fmaf(w1.w, x[3].y, fmaf(w1.z, x[2].y, fmaf(w1.y, x[1].y, w1.x * x[0].y))));
-      y[2] = silu(fmaf(w2.w, x[3].z, fmaf(w2.z, x[2].z, fmaf(w2.y, x[1].z, w2.x * x[0].z))));
-      y[3] = silu(fmaf(w3.w, x[3].w, fmaf(w3.z, x[2].w, fmaf(w3.y, x[1].w, w3.x * x[0].w))));
-      // the DK / 4 lanes of a q or k head are consecutive lanes of one wave
-      float ss = y[0] * y[0] + y[1] * y[1] + y[2] * y[2] + y[3] * y[3];
-      ss = group_sum<DK / 4>(ss);
+      float x[4][CPT];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) xr[u][w].get(x[w]);
+      if (code[u] < 0) {
+        // taps above the root read the conv-state slots (uniform; only near
+        // the start of a tree, as the canonical order sorts by depth)
+        const int i = g0 + u < np ? g0 + u : np - 1;
+#pragma unroll
+        for (int w = 0; w < 3; ++w) {
+          const int cd = __builtin_amdgcn_readfirstlane(s_tap[i][w]);
+          if (cd < 0) {
+#pragma unroll
+            for (int h = 0; h < CPT / 4; ++h) {
+              const float4 a = s_cs[-1 - cd][h][tid];
+              x[w][4 * h] = a.x, x[w][4 * h + 1] = a.y, x[w][4 * h + 2] = a.z, x[w][4 * h + 3] = a.w;
+            }
+          }
+        }
+      }
+      float y[CPT];
+      float ss = 0.0f;
+#pragma unroll
+      for (int j = 0; j < CPT; ++j) {
+        y[j] = silu(fmaf(wv[j].w, x[3][j], fmaf(wv[j].z, x[2][j], fmaf(wv[j].y, x[1][j], wv[j].x * x[0][j]))));
+        ss = fmaf(y[j], y[j], ss);
+      }
+      // the DK / CPT lanes of a q or k head are consecutive lanes of one wave
+      ss = group_sum<DK / CPT>(ss);
       const float f = qk ? rsqrt_hw(ss + 1e-6f) : 1.0f;
+      const bool st = ok && g0 + u < np;
       if constexpr (kHalf) {
         // v~: one power-of-two scale per (position, head) from the row max
-        float mx = fmaxf(fmaxf(fabsf(y[0]), fabsf(y[1])), fmaxf(fabsf(y[2]), fabsf(y[3])));
-        mx = group_max<VG>(mx);
+        float mx = 0.0f;
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) mx = fmaxf(mx, fabsf(y[j]));
+        mx = group_absmax<VG>(mx);
         float sc, inv;
         row_scale(mx, sc, inv);
-        if (ok && i0 + u < np) {
-          *reinterpret_cast<uint2*>(dsth + size_t(i0 + u) * C) =
-              to_f16x4(make_float4(y[0], y[1], y[2], y[3]), qk ? f : sc);
-          if (vs_lane) vs[size_t(i0 + u) * Hv] = inv;
+        const float g = qk ? f : sc;
+        uint2 h4[CPT / 4];
+#pragma unroll
+        for (int h = 0; h < CPT / 4; ++h) h4[h] = to_f16x4(make_float4(y[4 * h], y[4 * h + 1], y[4 * h + 2], y[4 * h + 3]), g);
+        if (st) {
+          if constexpr (CPT == 8)
+            *reinterpret_cast<uint4*>(dsth + size_t(g0 + u) * C) = make_uint4(h4[0].x, h4[0].y, h4[1].x, h4[1].y);
+          else
+            *reinterpret_cast<uint2*>(dsth + size_t(g0 + u) * C) = h4[0];
+          if (vs_lane) vs[size_t(g0 + u) * Hv] = inv;
         }
       } else {
-        if (ok && i0 + u < np)
-          *reinterpret_cast<float4*>(dst + size_t(i0 + u) * C) = make_float4(y[0] * f, y[1] * f, y[2] * f, y[3] * f);
+        if (st) {
+          float4* d4 = reinterpret_cast<float4*>(dst + size_t(g0 + u) * C);
+#pragma unroll
+          for (int h = 0; h < CPT / 4; ++h)
+            d4[h] = make_float4(y[4 * h] * f, y[4 * h + 1] * f, y[4 * h + 2] * f, y[4 * h + 3] * f);
+        }
       }
     }
+  };
+  load_group(ra, ca, 0);
+  for (int i0 = 0;;) {
+    load_group(rb, cb, i0 + kFU);
+    compute_group(ra, ca, i0);
+    i0 += kFU;
+    if (i0 >= np) break;
+    load_group(ra, ca, i0 + kFU);
+    compute_group(rb, cb, i0);
+    i0 += kFU;
+    if (i0 >= np) break;
   }
 }
 
@@ -464,9 +586,18 @@ __global__ __launch_bounds__(kLT) void pull_kernel(LargeParams p) {
 // ---------------------------------------------------------------------------
 // Launch
 // ---------------------------------------------------------------------------
-static dim3 feat_grid(const LargeParams& p, int dk, int dv, bool half) {
-  const int n4 = feat_vbase4(p.Hk, dk, half) + p.Hv * dv / 4;
-  return dim3((n4 + kFT - 1) / kFT, (p.T + kFP - 1) / kFP, p.B);
+// channels per thread of the feature kernel: 8 for the fp16 workspace, 4
+// for the fp32 features
+constexpr int kFCHalf = 8, kFCF32 = 4;
+
+// channel blocks of the feature kernel
+static int feat_cblocks(const LargeParams& p, int dk, int dv, int cpt) {
+  const int nt = feat_vbase(p.Hk, dk, cpt) + p.Hv * dv / cpt;
+  return (nt + kFT - 1) / kFT;
+}
+
+static dim3 feat_grid(const LargeParams& p, int dk, int dv, int cpt) {
+  return dim3(feat_cblocks(p, dk, dv, cpt) * ((p.T + kFP - 1) / kFP) * p.B);
 }
 
 template <int DK, int DV, typename TIn, bool FUSED>
@@ -494,7 +625,8 @@ static int launch_large_t(const LargeParams& p, bool fused, hipStream_t stream) 
     const int rc = launch_commit_conv(p.cp, DK, DV, std::is_same<TIn, BF16>::value ? GDN_BF16 : GDN_F32, stream);
     if (rc != GDN_OK) return rc;
   }
-  hipLaunchKernelGGL((feat_kernel<TIn, DK, DV / 4>), feat_grid(p, DK, DV, true), dim3(kFT), 0, stream, p, DV);
+  hipLaunchKernelGGL((feat_kernel<TIn, DK, DV / kFCHalf, kFCHalf>), feat_grid(p, DK, DV, kFCHalf), dim3(kFT), 0, stream,
+                     p, DV, feat_cblocks(p, DK, DV, kFCHalf));
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return set_error(GDN_EHIP, "verify (T > 128) feature launch: %s", hipGetErrorString(e));
   if constexpr (kCanFuse)
@@ -582,10 +714,14 @@ int launch_verify_large(const VerifyArgs& a, void* ws, size_t ws_bytes, hipStrea
 template <typename TIn>
 static int launch_features_t(const VerifyArgs& a, const LargeParams& p, hipStream_t stream) {
   switch (a.dk) {
-    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16, 0>), feat_grid(p, 16, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
-    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32, 0>), feat_grid(p, 32, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
-    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64, 0>), feat_grid(p, 64, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
-    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128, 0>), feat_grid(p, 128, a.dv, false), dim3(kFT), 0, stream, p, a.dv); break;
+    case 16: hipLaunchKernelGGL((feat_kernel<TIn, 16, 0, kFCF32>), feat_grid(p, 16, a.dv, kFCF32), dim3(kFT), 0, stream,
+                                  p, a.dv, feat_cblocks(p, 16, a.dv, kFCF32)); break;
+    case 32: hipLaunchKernelGGL((feat_kernel<TIn, 32, 0, kFCF32>), feat_grid(p, 32, a.dv, kFCF32), dim3(kFT), 0, stream,
+                                  p, a.dv, feat_cblocks(p, 32, a.dv, kFCF32)); break;
+    case 64: hipLaunchKernelGGL((feat_kernel<TIn, 64, 0, kFCF32>), feat_grid(p, 64, a.dv, kFCF32), dim3(kFT), 0, stream,
+                                  p, a.dv, feat_cblocks(p, 64, a.dv, kFCF32)); break;
+    case 128: hipLaunchKernelGGL((feat_kernel<TIn, 128, 0, kFCF32>), feat_grid(p, 128, a.dv, kFCF32), dim3(kFT), 0, stream,
+                                  p, a.dv, feat_cblocks(p, 128, a.dv, kFCF32)); break;
     default: return set_error(GDN_EUNSUPPORTED, "features: dk=%d unsupported", a.dk);
   }
   const hipError_t e = hipGetLastError();
