@@ -118,6 +118,21 @@ def test_deep_random_512(G, orc):
     _verify_commit(G, orc, w, "deep512")
 
 
+def test_shallow_wide_trees(G, orc):
+    """Every node within two levels of the root (a star of 300 nodes and a
+    root with 15 children of 20 children each): the conv taps above the
+    root are taken from the conv state in every position block."""
+    star = np.full(300, 0, np.int32)
+    star[0] = -1
+    two = np.full(300, -1, np.int32)
+    two[1:16] = 0
+    two[16:] = 1 + (np.arange(16, 300) - 16) % 15
+    w = W.make_random(7170, 2, 300, 2, 4, 64, 32, "bf16", parent=np.stack([star, two]))
+    assert np.any(w.conv_state != 0)
+    _announce("shallow wide trees T=300 (depth 1 and 2)")
+    _verify_commit(G, orc, w, "wide300")
+
+
 def test_chain_512(G, orc):
     """A single 512-node path (depth 511): the longest walks and a commit of
     the whole chain (16 feature chunks)."""
