@@ -27,6 +27,7 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
   __shared__ __align__(16) int s_dep[kMaxT];
   __shared__ __align__(16) uint64_t s_anc[kMaxT * KW];
   __shared__ int s_bad, s_roots, s_real, s_cycle;
+  __shared__ int s_more[2];  // a jump of this round is not at a root yet (rounds alternate)
 
   const int b = blockIdx.x;
   const int i = threadIdx.x;
@@ -38,6 +39,7 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
     s_roots = 0;
     s_real = 0;
     s_cycle = 0;
+    s_more[0] = 0;
   }
   int p = slot ? parent[size_t(b) * T + i] : kPad;
   if (slot) s_par[i] = p;
@@ -71,7 +73,7 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
 #pragma unroll
   for (int w = 0; w < KW; ++w)
     if (nxt >= 0 && w == (nxt >> 6)) anc[w] |= 1ull << (nxt & 63);
-  for (int span = 1; span < T; span <<= 1) {
+  for (int span = 1, r = 0; span < T; span <<= 1, r ^= 1) {
     if (slot) {
       s_nxt[i] = nxt;
       s_dep[i] = dep;
@@ -79,6 +81,8 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
       for (int w = 0; w < KW; ++w) s_anc[i * KW + w] = anc[w];
     }
     __syncthreads();
+    // the other round's flag was last read before the barrier above
+    if (i == 0) s_more[r ^ 1] = 0;
     if (nxt >= 0) {
       int j = nxt;
       dep += s_dep[j];
@@ -86,7 +90,11 @@ __global__ __launch_bounds__(kPrepMaxT) void prepare_kernel(const int32_t* __res
       for (int w = 0; w < KW; ++w) anc[w] |= s_anc[j * KW + w];
       nxt = s_nxt[j];
     }
+    if (nxt >= 0) s_more[r] = 1;
     __syncthreads();
+    // every jump reached a root: the remaining rounds would change nothing
+    // (a cycle never gets there and keeps jumping until span >= T)
+    if (!s_more[r]) break;
   }
   if (status == GDN_TREE_OK && real && nxt >= 0) s_cycle = 1;
   __syncthreads();
