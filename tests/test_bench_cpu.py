@@ -62,3 +62,19 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.returncode == 2
     assert "exactly one GPU" in r.stderr
     assert r.stdout.strip() == ""
+
+
+def test_traffic_is_gated_on_the_kernel_source():
+    """The HBM bytes quoted with the roofline come from the committed counter
+    summary only while it was taken on the current verify / step source."""
+    h = bench.verify_source_hash()
+    got = bench.measured_traffic(h, "step", "large")
+    with open(os.path.join(ROOT, "profiles", "step_large_hbm_traffic.md")) as f:
+        text = f.read()
+    if f"`{h}`" in text:
+        assert got is not None and 4.0e8 < got < 4.6e8   # 1.0-1.15 x the 401.7 MB of the step
+    else:
+        assert got is None
+    assert bench.measured_traffic("0" * 16, "step", "large") is None
+    assert bench.measured_traffic(h, "verify", "large") is None or "verify" in open(
+        os.path.join(ROOT, "profiles", "verify_large_hbm_traffic.md")).read()
