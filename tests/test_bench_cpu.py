@@ -76,5 +76,5 @@ def test_traffic_is_gated_on_the_kernel_source():
     else:
         assert got is None
     assert bench.measured_traffic("0" * 16, "step", "large") is None
-    assert bench.measured_traffic(h, "verify", "large") is None or "verify" in open(
-        os.path.join(ROOT, "profiles", "verify_large_hbm_traffic.md")).read()
+    gv = bench.measured_traffic(h, "verify", "large")
+    assert gv is None or 2.9e8 < gv < 3.35e8             # 1.0-1.15 x the 290.2 MB of the verify
