@@ -208,11 +208,26 @@ __global__ __launch_bounds__(kHT) void chunk_kernel(ChunkParams p) {
     s_be[j] = real ? ld(beta, (bt + nd) * Hv + h) : 0.0f;
   }
   __syncthreads();
-  // log a_p: sum of log alpha over the path root..p
-  for (int j = tid; j < T; j += kHT) {
-    float sl = 0.0f;
-    for (int t = j < nval ? j : -1; t >= 0; t = s_ppos[t]) sl += s_lal[t];
-    s_la[j] = sl;
+  // log a_p: sum of log alpha over the path root..p, by pointer jumping
+  // (ceil(log2 T) rounds instead of a walk of depth(p) steps per position;
+  // s_lal and s_ppos are rewritten to partial sums and 2^r-th ancestors)
+  static_assert(kHT >= kHMaxT, "one position per thread");
+  {
+    float sl = tid < T ? s_lal[tid] : 0.0f;
+    int nx = tid < T ? s_ppos[tid] : -1;
+    for (int span = 1; span < T; span <<= 1) {
+      if (nx >= 0) {
+        sl += s_lal[nx];
+        nx = s_ppos[nx];
+      }
+      __syncthreads();
+      if (tid < T) {
+        s_lal[tid] = sl;
+        s_ppos[tid] = int16_t(nx);
+      }
+      __syncthreads();
+    }
+    if (tid < T) s_la[tid] = sl;
   }
   if (nval > 0) {
     const float* S0 = p.S0 + (size_t(b) * Hv + h) * size_t(DV) * DK;

@@ -19,3 +19,11 @@ def test_instrumentation_anchors_match_the_kernel():
     for _, a, b in P.PHASES:
         for k in (a, b):
             assert any(s.startswith(f"TS({k}") for s in stamps), k
+
+
+def test_chunked_instrumentation_anchors_match_the_kernel():
+    with open(os.path.join(ROOT, "paper_2607_06763_amd", "csrc", "gdn_chunked.hip")) as f:
+        out = P._instrument_chunked(f.read())
+    stamps = [ln.strip() for ln in out.splitlines() if ln.strip().startswith("TS(")]
+    assert len(stamps) == 8           # metadata, phase A, phase B, 4 per block, end
+    assert "TS(127);" in stamps and 'extern "C" void gdn_chunk_stamps' in out
