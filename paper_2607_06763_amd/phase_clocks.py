@@ -54,9 +54,12 @@ def _instrument(src: str) -> str:
         "#define TS(k) do { const long long lin_ = ((long long)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + "
         "blockIdx.x; if (p.stamps && lin_ < p.stamp_cap && (threadIdx.x & 63) == 0 && (threadIdx.x >> 6) < 8 && "
         "(k) < 64) p.stamps[lin_ * 512 + (threadIdx.x >> 6) * 64 + (k)] = __builtin_amdgcn_s_memtime(); } while (0)\n"
-        "static unsigned long long* g_stamps = nullptr;\nstatic long long g_stamp_cap = 0;\n")
+        "static unsigned long long* g_stamps = nullptr;\nstatic long long g_stamp_cap = 0;\n"
+        "#define TR(k) do { const long long lin_ = ((long long)blockIdx.z * gridDim.y + blockIdx.y) * gridDim.x + "
+        "blockIdx.x; if (p.stamps && lin_ < p.stamp_cap && threadIdx.x == 0) "
+        "p.stamps[lin_ * 512 + (k)] = __builtin_amdgcn_s_memrealtime(); } while (0)\n")
     rep("  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;\n",
-        "  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;\n  TS(0);\n")
+        "  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;\n  TS(0);\n  TR(62);\n")
     rep("  // ---------------- phase 2: one value head at a time ----------------\n",
         "  TS(1);\n  // ---------------- phase 2: one value head at a time ----------------\n")
     rep("    if constexpr (FUSED) fused_commit<DK, DVS, TIn>(p, s_rv, s_ppath, Lp, b, g, h, c0, tid, sr);\n",
@@ -73,7 +76,7 @@ def _instrument(src: str) -> str:
     rep("    lds_barrier();\n\n    // 2e: P^T", "    lds_barrier();\n    TS(8 + 8 * hh);\n\n    // 2e: P^T")
     rep("    lds_barrier();  // S0 planes consumed before the next head reuses the region\n  }\n",
         "    TS(9 + 8 * hh);\n    lds_barrier();  // S0 planes consumed before the next head reuses the region\n  }\n"
-        "  TS(40);\n")
+        "  TS(40);\n  TR(63);\n")
     rep("  p.commit_status = a.commit_status;\n",
         "  p.commit_status = a.commit_status;\n  p.stamps = g_stamps;\n  p.stamp_cap = g_stamp_cap;\n")
     src += ('\nextern "C" void gdn_phase_stamps(void* buf, long long cap_blocks) {\n'
@@ -271,6 +274,13 @@ def _run_step(args, G, W, np, torch, ctypes) -> int:
             dm = np.where(ok, d, 0).max(axis=1)
             print(f"| {name} | {'' if hh is None else hh} | {d0.mean():.0f} | {dm.mean():.0f} |")
     print(f"| whole workgroup (wave 0) | | {total0.mean():.0f} | |")
+    # s_memrealtime counts a constant 100 MHz: the ratio of the two counters
+    # over the same span is the shader clock the stamps count
+    real = st[:, 0, 63] - st[:, 0, 62]
+    ok = real > 0
+    if ok.any():
+        ghz = (total0[ok] / real[ok]).mean() * 0.1
+        print(f"shader clock over the workgroups' lifetimes: {ghz:.2f} GHz (s_memtime / s_memrealtime x 100 MHz)")
     return 0
 
 

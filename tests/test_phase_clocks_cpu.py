@@ -13,6 +13,7 @@ def test_instrumentation_anchors_match_the_kernel():
     out = P._instrument(src)
     stamps = [ln.strip() for ln in out.splitlines() if ln.strip().startswith("TS(")]
     assert len(stamps) == 11          # prologue 2, per head 8, end 1
+    assert out.count("TR(6") == 2      # real-time counter at the start and the end
     assert "TS(40);" in stamps
     assert "unsigned long long* stamps;" in out and 'extern "C" void gdn_phase_stamps' in out
     # every phase boundary the summary reads is stamped
